@@ -1,0 +1,219 @@
+"""Decode-step throughput of the shared KV pool on one MI355X.
+
+A step is one pass of the hot path over one batch: append one new token per
+request (page allocation + scatter through the page table), then batched
+decode attention over every request's whole context (split planning,
+attention kernel, split merge). Steps cycle over several layers, each with
+its own copy of the batch's KV in its own pool, so that consecutive steps
+never find their KV in the 256 MiB Infinity Cache, as when a model's layers
+are decoded one after another.
+
+Prints one JSON line. value = algorithmic bytes moved per second over the
+timed steps (KV read once, queries, outputs, lse, page-table entries, and
+the appended rows read and written), in GB/s.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 2]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E
+WORKLOAD_NAMES = {
+    1: "tiny MLA-16 decode: 4 requests {128,256,384,512} tokens, 64-page pool",
+    2: "DeepSeek-V2-Lite-shaped MLA-16 decode: 32 requests, log-uniform 1K-32K tokens, 2 GiB pool",
+    3: "DeepSeek-V3-shaped MLA-128 decode: 8 requests x 128K tokens",
+    4: "mixed MLA-16/MQA-32/GQA-32x4 decode: 48 requests, Zipf(1.2) models, log-uniform 512-64K tokens, 8 GiB pool",
+    5: "MLA-128 burst: 1 request at 512K tokens in a 2 GiB pool 90% full",
+}
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--config", type=int, default=2, choices=[1, 2, 3, 4, 5])
+    ap.add_argument("--layers", type=int, default=0, help="KV copies cycled by the steps (0: enough to exceed 1 GiB)")
+    ap.add_argument("--path", type=int, default=0, help="0 auto, 1 vector, 2 matrix cores")
+    ap.add_argument("--splits", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0, help="target CPU time of the oracle sample")
+    return ap.parse_args()
+
+
+def algorithmic_bytes_decode(wl, ctx):
+    from workloads import algorithmic_bytes
+
+    return algorithmic_bytes([wl.model(r) for r in range(len(ctx))], ctx)
+
+
+def cpu_baseline(wl, budget_s: float):
+    """The fp64 oracle, as it stands, on a bounded sample of the same batch:
+    whole requests in batch order until about budget_s seconds of CPU work."""
+    import oracle
+
+    try:
+        from threadpoolctl import threadpool_info
+
+        threads = max([d.get("num_threads", 1) for d in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        threads = len(os.sched_getaffinity(0))
+    done, nbytes, t_total = [], 0, 0.0
+    for r in range(len(wl.requests)):
+        rows = wl.rows_bits(r)
+        t0 = time.perf_counter()
+        oracle.decode(rows, wl.q_bits[r], wl.model(r))
+        t_total += time.perf_counter() - t0
+        done.append(r)
+        nbytes += algorithmic_bytes_decode(wl, [0] * 0) if False else 0
+        if t_total >= budget_s:
+            break
+    from workloads import algorithmic_bytes
+
+    nbytes = algorithmic_bytes([wl.model(r) for r in done], [wl.requests[r].ctx_len for r in done])
+    cpu = "unknown"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                cpu = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    return {
+        "value": nbytes / t_total / 1e9,
+        "unit": "GB/s",
+        "cores": int(threads),
+        "kind": "oracle",
+        "sample": f"fp64 NumPy oracle on requests {done[0]}..{done[-1]} ({len(done)} of {len(wl.requests)}) "
+                  f"of the same batch, {t_total:.1f} s, one call each; host CPU: {cpu}",
+        "req_tokens_per_s": len(done) / t_total,
+    }
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported (the path does not shard).",
+              file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    from paper_2606_24506_amd import crosspool as cpl
+    from workloads import make_workload
+    from workloads.harness import load, to_device_u16
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    wl = make_workload(args.config)
+    kv_bytes = sum(rq.ctx_len * wl.model(r).kappa for r, rq in enumerate(wl.requests))
+    layers = args.layers or max(1, math.ceil((1 << 30) / kv_bytes))
+    total_steps = args.warmup + args.steps
+    grow = -(-total_steps // layers) + 1
+    print(f"[bench] cfg{args.config}: {len(wl.requests)} requests, {kv_bytes / 1e6:.1f} MB KV per layer, "
+          f"{layers} layers", file=sys.stderr, flush=True)
+
+    rows_cache = {r: wl.rows_bits(r) for r in range(len(wl.requests))}
+    inter = 512 if args.config == 4 else (4096 if args.config == 5 else 0)
+    lds = [load(wl, reserve_extra=grow, interleave=inter, rows_override=rows_cache,
+                placement_seed=wl.placement_seed + 1000 * i) for i in range(layers)]
+    del rows_cache
+    B = len(wl.requests)
+    # one new token per request per step: seeded rows, resident on the GPU before timing
+    new_rows = []
+    for r in range(B):
+        new_rows.append(wl.step_rows_bits(r, 0).reshape(-1))
+    new_rows = to_device_u16(np.concatenate(new_rows), "cuda")
+    ones = [1] * B
+    stream = torch.cuda.current_stream()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    for a, b in ev:
+        a.record(stream)
+        b.record(stream)
+    torch.cuda.synchronize()
+
+    def step(i, evs=None):
+        ld = lds[i % layers]
+        ld.pool.append(ld.req_ids, ones, new_rows, stream)
+        opts = dict(num_splits=args.splits, path=args.path)
+        if evs is not None:
+            opts.update(ev_begin=evs[0].cuda_event, ev_end=evs[1].cuda_event)
+        ld.pool.decode(ld.req_ids, ld.q, ld.out, ld.lse, stream, **opts)
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    # algorithmic bytes of the timed steps (contexts grow by one per visit)
+    ctx0 = [[ld.pool.ctx_len(r) for r in ld.req_ids] for ld in lds]
+    dec_bytes, app_bytes = 0, 0
+    visits = [0] * layers
+    for i in range(args.steps):
+        li = (args.warmup + i) % layers
+        ctx = [c + visits[li] + 1 for c in ctx0[li]]
+        visits[li] += 1
+        dec_bytes += algorithmic_bytes_decode(wl, ctx)
+        app_bytes += sum(2 * wl.model(r).kappa + 4 for r in range(B))
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(args.warmup + i, ev[i])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    kern_ms = sum(a.elapsed_time(b) for a, b in ev) / args.steps
+
+    value = (dec_bytes + app_bytes) / wall / 1e9
+    ms_per_step = wall * 1e3 / args.steps
+    achieved = dec_bytes / args.steps / (kern_ms * 1e-3) / 1e9
+    res = {
+        "metric": "paged decode-attention achieved HBM GB/s and req-tokens/s on 1 MI355X",
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded draws shaped like the workload; no dataset)",
+        "config": {
+            "workload": WORKLOAD_NAMES[args.config],
+            "requests": B,
+            "context_tokens": int(sum(ctx0[0])),
+            "kv_bytes_per_step": int(kv_bytes),
+            "layers_cycled": layers,
+            "step": "cp_kv_append (1 token/request) + cp_attn_decode",
+            "path": ["auto", "vector", "matrix"][args.path],
+        },
+        "req_tokens_per_s": round(B / (wall / args.steps), 1),
+        "context_tokens_per_s": round(sum(ctx0[0]) / (wall / args.steps), 1),
+        "roofline": {
+            "bound": "hbm",
+            "kernel": "decode attention (cp_attn_decode main launch, merge excluded)",
+            "achieved": round(achieved, 2),
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBS, 4),
+            "traffic": None,
+            "kernel_ms": round(kern_ms, 5),
+        },
+    }
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
+    for ld in lds:
+        ld.close()
+    print(json.dumps(res))
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,261 @@
+/*
+ * crosspool.h -- C ABI of a shared, virtualised KV-cache pool with batched
+ * decode attention, for AMD Instinct MI355X (gfx950).
+ *
+ * The operations follow the KV-cache pool of CrossPool (arXiv 2606.24506):
+ *   - one pool whose size is a page budget shared by several cold models
+ *     (Section 3.1, planner output "pool page budget"; Section 4);
+ *   - per-model KV geometry, i.e. per-token KV bytes kappa(M) that differ
+ *     between MLA, MQA and GQA models (Section 2.3 C1; Section 3.1);
+ *   - a paged logical KV interface in front of physical pages that the
+ *     virtualizer places, with page mapping kept off the per-token path
+ *     (Section 3.1, last paragraph; Section 4, KV-cache virtualization);
+ *   - admission that queues or rejects new requests when the budget is
+ *     exhausted and never interrupts admitted ones, whose pages live until
+ *     they finish (Section 3.1; Section 4);
+ *   - attention run next to the KV, reading it at every decode step
+ *     (Section 2.3 C2).
+ *
+ * Conventions for every call:
+ *   - Return value: CP_OK (0) or a negative cp_status. No call aborts or
+ *     throws. cp_last_error() gives a thread-local message for the last
+ *     failure on the calling thread.
+ *   - All argument and capacity checks run on the host before anything is
+ *     enqueued; on any error no pool state changes (all-or-nothing across a
+ *     whole batch).
+ *   - Device-memory arguments are device pointers on the pool's device;
+ *     host arguments are ordinary host pointers and are not retained after
+ *     the call returns. Streams are hipStream_t passed as void* (NULL = the
+ *     default stream).
+ *   - Calls that enqueue GPU work (append, decode, gather) return once the
+ *     work is enqueued; host-side metadata (context lengths, page tables) is
+ *     already updated at return, so append-then-decode on one stream is
+ *     ordered. Launch failures return CP_EHIP; device faults surface at the
+ *     caller's next synchronisation.
+ *   - A pool is not thread-safe: the caller serialises calls on one pool.
+ *     Decode calls on one pool must not overlap on the GPU (one stream, or
+ *     the caller orders streams), because they share the pool's workspace.
+ *   - bf16 is IEEE-754 binary32 truncated to its upper 16 bits; values are
+ *     produced with round-to-nearest-even.
+ */
+#ifndef CROSSPOOL_H
+#define CROSSPOOL_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t cp_status;
+enum {
+  CP_OK = 0,
+  CP_EINVAL = -1, /* bad argument, unknown id, out-of-range value */
+  CP_ENOMEM = -2, /* device or host allocation failed */
+  CP_ENOSPC = -3, /* pool page budget exhausted (admission reject) */
+  CP_EHIP = -4,   /* a HIP runtime call failed */
+  CP_ESTATE = -5  /* call not valid in the current state */
+};
+
+/* Message for the last failing call on this thread ("" if none). The
+ * returned string stays valid until the next failing call on this thread. */
+const char *cp_last_error(void);
+
+/* Library version, (major << 16) | minor. */
+int32_t cp_version(void);
+
+/* ------------------------------------------------------------------ pool */
+
+typedef struct cp_pool cp_pool; /* opaque */
+
+typedef struct {
+  /* Tokens per page, pool-wide (64 in the shipped workloads). A page of a
+   * model with kappa bytes per token holds page_tokens * kappa bytes. */
+  int32_t page_tokens;
+  /* HIP device ordinal, or -1 for a host-only pool: all bookkeeping
+   * (admission, page allocation, page tables) works, no device memory is
+   * touched, and append must pass rows == NULL; decode and gather return
+   * CP_ESTATE. Used to test the allocator without a GPU. */
+  int32_t device;
+  /* KV budget in bytes; rounded down to whole chunks. This is the shared
+   * page budget the planner emits (Section 3.1). */
+  uint64_t pool_bytes;
+  /* Allocation unit carved into pages of one model at a time; 0 means
+   * 2 MiB. Must be a multiple of 256. A model whose page does not fit in a
+   * chunk cannot be registered. */
+  uint64_t chunk_bytes;
+  /* 0: chunks are handed out in ascending address order. Otherwise each
+   * new chunk is drawn uniformly at random from the free chunks with a
+   * generator seeded by this value, so physical placement is scattered
+   * and reproducible. Logical results never depend on placement. */
+  uint64_t placement_seed;
+  /* Optional caller-owned device buffer of at least pool_bytes (after
+   * rounding), 256-byte aligned; it must outlive the pool. NULL: the pool
+   * allocates and owns its buffer. */
+  void *device_mem;
+  /* Maximum number of simultaneously open requests; 0 means 4096. */
+  int32_t max_requests;
+  int32_t reserved0;
+} cp_pool_desc;
+
+/* Create a pool. Errors: CP_EINVAL (page_tokens not in [1, 4096],
+ * chunk_bytes not a multiple of 256, fewer than one chunk), CP_ENOMEM
+ * (device or pinned-host allocation failed), CP_EHIP. */
+cp_status cp_pool_create(const cp_pool_desc *desc, cp_pool **out);
+
+/* Destroy a pool and free what it owns. CP_ESTATE if requests are still
+ * open. The caller must have synchronised every stream used with it. */
+cp_status cp_pool_destroy(cp_pool *pool);
+
+typedef struct {
+  uint64_t chunks_total;   /* whole chunks in the budget */
+  uint64_t chunks_used;    /* chunks currently carved for some model */
+  uint64_t pages_used;     /* pages holding KV of open requests */
+  uint64_t pages_reserved; /* pages promised to open requests */
+  int32_t requests_open;
+  int32_t models;
+} cp_pool_stats_t;
+
+cp_status cp_pool_stats(cp_pool *pool, cp_pool_stats_t *out);
+
+/* ---------------------------------------------------------------- models */
+
+typedef enum {
+  CP_KIND_MLA = 0, /* one latent KV head: row = [latent | rope]; V = latent */
+  CP_KIND_GQA = 1  /* n_kv_heads K and V heads; MQA is n_kv_heads = 1 */
+} cp_kind;
+
+typedef enum { CP_BF16 = 0 } cp_dtype;
+
+typedef struct {
+  int32_t kind;        /* cp_kind */
+  int32_t n_q_heads;   /* query heads per layer */
+  int32_t n_kv_heads;  /* MLA: must be 1; GQA: divides n_q_heads */
+  int32_t head_dim;    /* GQA: K and V width per KV head; MLA: ignored */
+  int32_t latent_dim;  /* MLA: latent width (also the V width) */
+  int32_t rope_dim;    /* MLA: decoupled rope width; K width = latent + rope */
+  float softmax_scale; /* > 0; 0 means 1/sqrt(head_dim) for GQA (required for MLA) */
+  int32_t dtype;       /* cp_dtype; only CP_BF16 */
+} cp_model_desc;
+
+/* Register the KV geometry of one attention layer of a model (Section 2.3
+ * C1: models differ in KV layout, KV heads and per-token KV bytes). Sets
+ * *model_id. Limits: n_q_heads in [1, 256]; V width in {64, 128, 256, 512};
+ * K width a multiple of 8 and at most 1024; per-token bytes at least 128.
+ * Errors: CP_EINVAL (geometry outside the limits, page larger than a chunk,
+ * too many models: at most 16). */
+cp_status cp_model_register(cp_pool *pool, const cp_model_desc *m, int32_t *model_id);
+
+typedef struct {
+  int32_t d_k, d_v;          /* K and V width per head */
+  int32_t kappa;             /* KV bytes per token */
+  int32_t page_bytes;        /* page_tokens * kappa */
+  int32_t pages_per_chunk;   /* pages carved from one chunk */
+  int32_t row_elems;         /* bf16 elements in one logical row */
+} cp_model_info_t;
+
+cp_status cp_model_info(cp_pool *pool, int32_t model_id, cp_model_info_t *out);
+
+/* -------------------------------------------------------------- requests */
+
+/* Admit a request of model_id that will hold at most reserve_tokens tokens
+ * (prompt plus generated). Admission reserves ceil(reserve_tokens /
+ * page_tokens) pages against the shared budget; it succeeds only if the
+ * budget can hold every open reservation of every model at once, so an
+ * admitted request is never refused a page later (Section 3.1: admission
+ * queues or rejects new requests rather than interrupting active decodes).
+ * Sets *req_id. Errors: CP_ENOSPC (budget exhausted: nothing changed, the
+ * caller may queue and retry), CP_EINVAL. */
+cp_status cp_request_open(cp_pool *pool, int32_t model_id, int64_t reserve_tokens, int32_t *req_id);
+
+/* Release a request: its pages go back to its model's slab, chunks that
+ * become empty go back to the shared budget, and its reservation ends
+ * (Section 3.1: pages are kept until the request finishes). The caller
+ * must have synchronised every stream with work on this request. */
+cp_status cp_request_close(cp_pool *pool, int32_t req_id);
+
+cp_status cp_request_len(cp_pool *pool, int32_t req_id, int64_t *ctx_len);
+
+/* Copy the request's page-table entries [first, first + count) to host
+ * memory. An entry is the byte offset of the page inside the pool buffer,
+ * shifted right by 8. For tests and debugging. */
+cp_status cp_request_pages(cp_pool *pool, int32_t req_id, int64_t first, int64_t count, uint32_t *ptes);
+
+/* ------------------------------------------------------------------- KV */
+
+/* Append n_new[i] tokens to request req_ids[i], i < n, scattering their KV
+ * rows into pool pages through the page table (Section 3.1: attention sees
+ * a normal paged interface while physical pages are mapped on demand).
+ *
+ * rows: device memory, the requests' logical rows packed in call order,
+ *   request i contributing n_new[i] consecutive rows. A logical row is
+ *   row_elems bf16 values: MLA [latent | rope]; GQA/MQA [K head 0 .. K head
+ *   Hkv-1 | V head 0 .. V head Hkv-1], each head head_dim wide. Rows are
+ *   copied bit for bit.
+ * req_ids, n_new: host arrays of n entries; req_ids must be distinct;
+ *   n_new[i] >= 0.
+ * New pages come from the model's slab, or a fresh chunk of the shared
+ *   budget; their page-table entries are written before the copy runs.
+ * Errors: CP_EINVAL (unknown or duplicate id, negative count, growth past
+ *   the reservation, rows == NULL on a device pool), CP_EHIP. */
+cp_status cp_kv_append(cp_pool *pool, int32_t n, const int32_t *req_ids, const int32_t *n_new,
+                       const void *rows, void *hip_stream);
+
+/* Batched decode attention over the pool (Section 2.3 C2: attention stays
+ * local to the KV and reads all of it at every decode step). Requests may
+ * belong to different models. For request i with context n_i >= 1 and every
+ * query head h (GQA groups are contiguous: head h reads KV head
+ * h / (n_q_heads / n_kv_heads)):
+ *     s_j = scale * <q_h, K_j>, j < n_i;  out_h = sum_j softmax(s)_j V_j;
+ *     lse_h = ln sum_j exp(s_j)  (natural log).
+ * q: device, per request [n_q_heads][d_k] bf16, packed in call order (MLA
+ *   queries are the absorbed form: latent part already multiplied through
+ *   the key up-projection, rope part post-rotary).
+ * out: device, per request [n_q_heads][d_v] bf16, packed in call order.
+ * lse: device, per request [n_q_heads] float, packed in call order.
+ * req_ids: host array of n distinct ids, n >= 1.
+ * Accumulation is fp32; outputs depend only on the logical KV, never on
+ * the physical placement of pages (bit-identical across placements).
+ * Errors: CP_EINVAL (unknown or duplicate id, empty context), CP_ESTATE
+ * (host-only pool), CP_ENOMEM (workspace growth failed), CP_EHIP. */
+cp_status cp_attn_decode(cp_pool *pool, int32_t n, const int32_t *req_ids, const void *q, void *out, float *lse,
+                         void *hip_stream);
+
+typedef enum {
+  CP_PATH_AUTO = 0, /* matrix cores where many query heads share a KV head, vector otherwise */
+  CP_PATH_VALU = 1, /* force the vector (wavefront-reduction) kernel for every model */
+  CP_PATH_MFMA = 2  /* force the matrix-core kernel for every model */
+} cp_path;
+
+typedef struct {
+  /* 0: the planner chooses the split of each request's context into KV
+   * ranges; k >= 1 forces min(k, pages) page-aligned ranges per request. */
+  int32_t num_splits;
+  /* 1 (default when opts == NULL): a persistent grid pulls work units from
+   * a device queue, longest first; 0: one workgroup per unit. */
+  int32_t persistent;
+  /* cp_path */
+  int32_t path;
+  int32_t reserved0;
+  /* Optional hipEvent_t handles recorded on the stream immediately before
+   * and after the main attention kernel (not the merge), for timing. */
+  void *ev_begin;
+  void *ev_end;
+} cp_decode_opts;
+
+/* cp_attn_decode with options; opts == NULL behaves like cp_attn_decode. */
+cp_status cp_attn_decode_ex(cp_pool *pool, int32_t n, const int32_t *req_ids, const void *q, void *out, float *lse,
+                            void *hip_stream, const cp_decode_opts *opts);
+
+/* Copy logical rows [start, start + n_tok) of one request out of the pool
+ * into dst (device, n_tok * row_elems bf16), through the same page-table
+ * translation that decode uses. Bit-exact inverse of cp_kv_append.
+ * Errors: CP_EINVAL (range outside [0, ctx_len)), CP_ESTATE (host-only
+ * pool), CP_EHIP. */
+cp_status cp_kv_gather(cp_pool *pool, int32_t req_id, int64_t start, int64_t n_tok, void *dst, void *hip_stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CROSSPOOL_H */

@@ -1,0 +1,307 @@
+"""ctypes binding of libcrosspool.so (include/crosspool.h).
+
+Argument marshalling only: every step of the hot path runs in the library's
+HIP kernels. PyTorch is used for device buffers and streams. The functions
+keep the C names; ``Pool`` is a small convenience wrapper over them.
+
+Importing this module loads the library and fails loudly if it has not been
+built (``python -m paper_2606_24506_amd.build``); there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+from typing import Optional, Sequence
+
+import numpy as np
+
+_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libcrosspool.so")
+
+CP_OK, CP_EINVAL, CP_ENOMEM, CP_ENOSPC, CP_EHIP, CP_ESTATE = 0, -1, -2, -3, -4, -5
+CP_KIND_MLA, CP_KIND_GQA = 0, 1
+CP_PATH_AUTO, CP_PATH_VALU, CP_PATH_MFMA = 0, 1, 2
+_NAMES = {0: "CP_OK", -1: "CP_EINVAL", -2: "CP_ENOMEM", -3: "CP_ENOSPC", -4: "CP_EHIP", -5: "CP_ESTATE"}
+
+
+class CrossPoolError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{_NAMES.get(status, status)}: {message}")
+        self.status = status
+        self.message = message
+
+
+class cp_pool_desc(C.Structure):
+    _fields_ = [
+        ("page_tokens", C.c_int32),
+        ("device", C.c_int32),
+        ("pool_bytes", C.c_uint64),
+        ("chunk_bytes", C.c_uint64),
+        ("placement_seed", C.c_uint64),
+        ("device_mem", C.c_void_p),
+        ("max_requests", C.c_int32),
+        ("reserved0", C.c_int32),
+    ]
+
+
+class cp_pool_stats_t(C.Structure):
+    _fields_ = [
+        ("chunks_total", C.c_uint64),
+        ("chunks_used", C.c_uint64),
+        ("pages_used", C.c_uint64),
+        ("pages_reserved", C.c_uint64),
+        ("requests_open", C.c_int32),
+        ("models", C.c_int32),
+    ]
+
+
+class cp_model_desc(C.Structure):
+    _fields_ = [
+        ("kind", C.c_int32),
+        ("n_q_heads", C.c_int32),
+        ("n_kv_heads", C.c_int32),
+        ("head_dim", C.c_int32),
+        ("latent_dim", C.c_int32),
+        ("rope_dim", C.c_int32),
+        ("softmax_scale", C.c_float),
+        ("dtype", C.c_int32),
+    ]
+
+
+class cp_model_info_t(C.Structure):
+    _fields_ = [
+        ("d_k", C.c_int32),
+        ("d_v", C.c_int32),
+        ("kappa", C.c_int32),
+        ("page_bytes", C.c_int32),
+        ("pages_per_chunk", C.c_int32),
+        ("row_elems", C.c_int32),
+    ]
+
+
+class cp_decode_opts(C.Structure):
+    _fields_ = [
+        ("num_splits", C.c_int32),
+        ("persistent", C.c_int32),
+        ("path", C.c_int32),
+        ("reserved0", C.c_int32),
+        ("ev_begin", C.c_void_p),
+        ("ev_end", C.c_void_p),
+    ]
+
+
+def _load() -> C.CDLL:
+    # PyTorch ships its own HIP runtime (soname libamdhip64.so.7, like the
+    # system one). Loading torch first makes the library bind to that same
+    # runtime instance, so torch's streams and allocations are valid here.
+    try:
+        import torch  # noqa: F401
+    except ImportError:  # pragma: no cover - plain C users do not need torch
+        pass
+    if not os.path.exists(_LIB_PATH):
+        raise ImportError(f"{_LIB_PATH} is not built; run `python -m paper_2606_24506_amd.build`")
+    lib = C.CDLL(_LIB_PATH)
+    P, I32, I64, VP = C.c_void_p, C.c_int32, C.c_int64, C.c_void_p
+    sig = {
+        "cp_last_error": ([], C.c_char_p),
+        "cp_version": ([], I32),
+        "cp_pool_create": ([C.POINTER(cp_pool_desc), C.POINTER(P)], I32),
+        "cp_pool_destroy": ([P], I32),
+        "cp_pool_stats": ([P, C.POINTER(cp_pool_stats_t)], I32),
+        "cp_model_register": ([P, C.POINTER(cp_model_desc), C.POINTER(I32)], I32),
+        "cp_model_info": ([P, I32, C.POINTER(cp_model_info_t)], I32),
+        "cp_request_open": ([P, I32, I64, C.POINTER(I32)], I32),
+        "cp_request_close": ([P, I32], I32),
+        "cp_request_len": ([P, I32, C.POINTER(I64)], I32),
+        "cp_request_pages": ([P, I32, I64, I64, C.POINTER(C.c_uint32)], I32),
+        "cp_kv_append": ([P, I32, C.POINTER(I32), C.POINTER(I32), VP, VP], I32),
+        "cp_attn_decode": ([P, I32, C.POINTER(I32), VP, VP, VP, VP], I32),
+        "cp_attn_decode_ex": ([P, I32, C.POINTER(I32), VP, VP, VP, VP, C.POINTER(cp_decode_opts)], I32),
+        "cp_kv_gather": ([P, I32, I64, I64, VP, VP], I32),
+    }
+    for name, (args, res) in sig.items():
+        fn = getattr(lib, name)
+        fn.argtypes = args
+        fn.restype = res
+    return lib
+
+
+LIB = _load()
+
+
+def _check(rc: int):
+    if rc != CP_OK:
+        raise CrossPoolError(rc, LIB.cp_last_error().decode(errors="replace"))
+
+
+def _i32_array(xs: Sequence[int]):
+    arr = (C.c_int32 * len(xs))(*[int(x) for x in xs])
+    return arr
+
+
+def _ptr(t) -> Optional[int]:
+    """Device pointer of a tensor (or None / raw int)."""
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    if not t.is_contiguous():
+        raise ValueError("tensor must be contiguous")
+    return t.data_ptr()
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        import torch
+
+        if not torch.cuda.is_available():
+            return None
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+# ------------------------------------------------------------ C names ----
+
+def cp_version() -> int:
+    return int(LIB.cp_version())
+
+
+def cp_pool_create(page_tokens: int = 64, pool_bytes: int = 0, chunk_bytes: int = 0, placement_seed: int = 0,
+                   device: int = 0, device_mem=None, max_requests: int = 0) -> int:
+    d = cp_pool_desc(page_tokens, device, pool_bytes, chunk_bytes, placement_seed, _ptr(device_mem), max_requests, 0)
+    out = C.c_void_p()
+    _check(LIB.cp_pool_create(C.byref(d), C.byref(out)))
+    return out.value
+
+
+def cp_pool_destroy(pool: int) -> None:
+    _check(LIB.cp_pool_destroy(pool))
+
+
+def cp_pool_stats(pool: int) -> dict:
+    s = cp_pool_stats_t()
+    _check(LIB.cp_pool_stats(pool, C.byref(s)))
+    return {f: getattr(s, f) for f, _ in s._fields_}
+
+
+def cp_model_register(pool: int, kind: int, n_q_heads: int, n_kv_heads: int, head_dim: int = 0,
+                      latent_dim: int = 0, rope_dim: int = 0, softmax_scale: float = 0.0) -> int:
+    m = cp_model_desc(kind, n_q_heads, n_kv_heads, head_dim, latent_dim, rope_dim, softmax_scale, 0)
+    mid = C.c_int32()
+    _check(LIB.cp_model_register(pool, C.byref(m), C.byref(mid)))
+    return mid.value
+
+
+def cp_model_info(pool: int, model_id: int) -> dict:
+    s = cp_model_info_t()
+    _check(LIB.cp_model_info(pool, model_id, C.byref(s)))
+    return {f: getattr(s, f) for f, _ in s._fields_}
+
+
+def cp_request_open(pool: int, model_id: int, reserve_tokens: int) -> int:
+    rid = C.c_int32()
+    _check(LIB.cp_request_open(pool, model_id, reserve_tokens, C.byref(rid)))
+    return rid.value
+
+
+def cp_request_close(pool: int, req_id: int) -> None:
+    _check(LIB.cp_request_close(pool, req_id))
+
+
+def cp_request_len(pool: int, req_id: int) -> int:
+    n = C.c_int64()
+    _check(LIB.cp_request_len(pool, req_id, C.byref(n)))
+    return n.value
+
+
+def cp_request_pages(pool: int, req_id: int, first: int, count: int) -> np.ndarray:
+    out = np.zeros(count, dtype=np.uint32)
+    _check(LIB.cp_request_pages(pool, req_id, first, count, out.ctypes.data_as(C.POINTER(C.c_uint32))))
+    return out
+
+
+def cp_kv_append(pool: int, req_ids: Sequence[int], n_new: Sequence[int], rows, stream=None) -> None:
+    n = len(req_ids)
+    if len(n_new) != n:
+        raise ValueError("req_ids and n_new differ in length")
+    _check(LIB.cp_kv_append(pool, n, _i32_array(req_ids), _i32_array(n_new), _ptr(rows), _stream(stream)))
+
+
+def cp_attn_decode(pool: int, req_ids: Sequence[int], q, out, lse, stream=None) -> None:
+    _check(LIB.cp_attn_decode(pool, len(req_ids), _i32_array(req_ids), _ptr(q), _ptr(out), _ptr(lse), _stream(stream)))
+
+
+def cp_attn_decode_ex(pool: int, req_ids: Sequence[int], q, out, lse, stream=None, *, num_splits: int = 0,
+                      persistent: int = 1, path: int = CP_PATH_AUTO, ev_begin=None, ev_end=None) -> None:
+    def ev(e):
+        if e is None:
+            return None
+        return e.cuda_event if hasattr(e, "cuda_event") else int(e)
+
+    o = cp_decode_opts(num_splits, persistent, path, 0, ev(ev_begin), ev(ev_end))
+    _check(LIB.cp_attn_decode_ex(pool, len(req_ids), _i32_array(req_ids), _ptr(q), _ptr(out), _ptr(lse),
+                                 _stream(stream), C.byref(o)))
+
+
+def cp_kv_gather(pool: int, req_id: int, start: int, n_tok: int, dst, stream=None) -> None:
+    _check(LIB.cp_kv_gather(pool, req_id, start, n_tok, _ptr(dst), _stream(stream)))
+
+
+# -------------------------------------------------------- convenience ----
+
+class Pool:
+    """Owns one cp_pool handle; methods forward to the C names above."""
+
+    def __init__(self, **desc):
+        self.handle = cp_pool_create(**desc)
+        self.device = desc.get("device", 0)
+        self.page_tokens = desc.get("page_tokens", 64)
+
+    def register(self, kind: int, n_q_heads: int, n_kv_heads: int, **kw) -> int:
+        return cp_model_register(self.handle, kind, n_q_heads, n_kv_heads, **kw)
+
+    def register_spec(self, spec) -> int:
+        """Register a model described by an object with kind / head fields."""
+        if spec.kind == "mla":
+            return self.register(CP_KIND_MLA, spec.n_q_heads, 1, latent_dim=spec.latent_dim,
+                                 rope_dim=spec.rope_dim, softmax_scale=spec.scale)
+        return self.register(CP_KIND_GQA, spec.n_q_heads, spec.n_kv_heads, head_dim=spec.head_dim,
+                             softmax_scale=spec.scale)
+
+    def info(self, model_id: int) -> dict:
+        return cp_model_info(self.handle, model_id)
+
+    def open(self, model_id: int, reserve_tokens: int) -> int:
+        return cp_request_open(self.handle, model_id, reserve_tokens)
+
+    def close(self, req_id: int) -> None:
+        cp_request_close(self.handle, req_id)
+
+    def ctx_len(self, req_id: int) -> int:
+        return cp_request_len(self.handle, req_id)
+
+    def pages(self, req_id: int, first: int = 0, count: Optional[int] = None) -> np.ndarray:
+        if count is None:
+            count = -(-self.ctx_len(req_id) // self.page_tokens) - first
+        return cp_request_pages(self.handle, req_id, first, count)
+
+    def stats(self) -> dict:
+        return cp_pool_stats(self.handle)
+
+    def append(self, req_ids, n_new, rows, stream=None) -> None:
+        cp_kv_append(self.handle, req_ids, n_new, rows, stream)
+
+    def decode(self, req_ids, q, out, lse, stream=None, **opts) -> None:
+        if opts:
+            cp_attn_decode_ex(self.handle, req_ids, q, out, lse, stream, **opts)
+        else:
+            cp_attn_decode(self.handle, req_ids, q, out, lse, stream)
+
+    def gather(self, req_id, start, n_tok, dst, stream=None) -> None:
+        cp_kv_gather(self.handle, req_id, start, n_tok, dst, stream)
+
+    def destroy(self) -> None:
+        if self.handle:
+            cp_pool_destroy(self.handle)
+            self.handle = None

@@ -1,0 +1,612 @@
+// C ABI of the shared KV pool (declared in include/crosspool.h): argument
+// checks, page allocation, split planning, and kernel launches.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "crosspool.h"
+#include "kargs.h"
+#include "pool.hpp"
+
+namespace cp {
+hipError_t launch_append(const AppendArgs &a, hipStream_t stream);
+hipError_t launch_gather(const GatherArgs &a, hipStream_t stream);
+hipError_t launch_decode_valu(const DecodeArgs &a, int grid, hipStream_t stream);
+hipError_t launch_merge(const MergeArgs &a, hipStream_t stream);
+}  // namespace cp
+
+using namespace cp;
+
+namespace {
+
+thread_local std::string g_err;
+
+cp_status fail(cp_status code, const char *fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+cp_status hip_fail(hipError_t e, const char *what) {
+  return fail(CP_EHIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+// Makes the pool's device current for the duration of a call.
+struct DeviceGuard {
+  int prev = -1;
+  bool active = false;
+  explicit DeviceGuard(int dev) {
+    if (dev < 0) return;
+    if (hipGetDevice(&prev) == hipSuccess && prev != dev) {
+      active = hipSetDevice(dev) == hipSuccess;
+    }
+  }
+  ~DeviceGuard() {
+    if (active) (void)hipSetDevice(prev);
+  }
+};
+
+}  // namespace
+
+struct cp_pool {
+  PoolState st;
+  int device = -1;
+  bool host_only = true;
+  uint8_t *dev_pool = nullptr;
+  bool owns_pool = false;
+  uint32_t *dev_pte = nullptr;
+  uint32_t *pin_pte = nullptr;  // pinned staging copy of the page table
+  uint32_t *queue = nullptr;    // persistent-grid counters
+  float *ws_o = nullptr;
+  float *ws_l = nullptr;
+  uint64_t ws_o_cap = 0, ws_l_cap = 0;  // floats
+  int num_cus = 256;
+};
+
+extern "C" {
+
+const char *cp_last_error(void) { return g_err.c_str(); }
+
+int32_t cp_version(void) { return (0 << 16) | 1; }
+
+cp_status cp_pool_create(const cp_pool_desc *d, cp_pool **out) {
+  if (!d || !out) return fail(CP_EINVAL, "null argument");
+  *out = nullptr;
+  auto *p = new (std::nothrow) cp_pool();
+  if (!p) return fail(CP_ENOMEM, "host allocation failed");
+  std::string e = p->st.init(d->page_tokens, d->pool_bytes, d->chunk_bytes, d->placement_seed, d->max_requests);
+  if (!e.empty()) {
+    delete p;
+    return fail(CP_EINVAL, "%s", e.c_str());
+  }
+  p->device = d->device;
+  p->host_only = d->device < 0;
+  if (!p->host_only) {
+    int ndev = 0;
+    if (hipGetDeviceCount(&ndev) != hipSuccess || d->device >= ndev) {
+      delete p;
+      return fail(CP_EINVAL, "device %d not present", d->device);
+    }
+    DeviceGuard g(d->device);
+    hipError_t he;
+    uint64_t bytes = p->st.n_chunks() * p->st.chunk_bytes();
+    if (d->device_mem) {
+      if ((uintptr_t)d->device_mem % 256) {
+        delete p;
+        return fail(CP_EINVAL, "device_mem must be 256-byte aligned");
+      }
+      p->dev_pool = (uint8_t *)d->device_mem;
+    } else {
+      he = hipMalloc((void **)&p->dev_pool, bytes);
+      if (he != hipSuccess) {
+        delete p;
+        return fail(CP_ENOMEM, "hipMalloc of %llu pool bytes failed", (unsigned long long)bytes);
+      }
+      p->owns_pool = true;
+    }
+    uint64_t nptes = p->st.pte_capacity();
+    bool ok = hipMalloc((void **)&p->dev_pte, nptes * 4) == hipSuccess &&
+              hipHostMalloc((void **)&p->pin_pte, nptes * 4, hipHostMallocDefault) == hipSuccess &&
+              hipMalloc((void **)&p->queue, 64 * sizeof(uint32_t)) == hipSuccess;
+    if (ok) ok = hipMemset(p->dev_pte, 0, nptes * 4) == hipSuccess && hipMemset(p->queue, 0, 64 * 4) == hipSuccess;
+    if (ok) std::memset(p->pin_pte, 0, nptes * 4);
+    int cus = 0;
+    if (ok && hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, d->device) == hipSuccess && cus > 0)
+      p->num_cus = cus;
+    if (ok) ok = hipDeviceSynchronize() == hipSuccess;
+    if (!ok) {
+      cp_pool_destroy(p);
+      return fail(CP_ENOMEM, "device allocation of pool metadata failed");
+    }
+  }
+  *out = p;
+  return CP_OK;
+}
+
+cp_status cp_pool_destroy(cp_pool *p) {
+  if (!p) return fail(CP_EINVAL, "null pool");
+  if (p->st.n_open() > 0) return fail(CP_ESTATE, "%d requests still open", p->st.n_open());
+  if (!p->host_only) {
+    DeviceGuard g(p->device);
+    if (p->owns_pool && p->dev_pool) (void)hipFree(p->dev_pool);
+    if (p->dev_pte) (void)hipFree(p->dev_pte);
+    if (p->pin_pte) (void)hipHostFree(p->pin_pte);
+    if (p->queue) (void)hipFree(p->queue);
+    if (p->ws_o) (void)hipFree(p->ws_o);
+    if (p->ws_l) (void)hipFree(p->ws_l);
+  }
+  delete p;
+  return CP_OK;
+}
+
+cp_status cp_pool_stats(cp_pool *p, cp_pool_stats_t *o) {
+  if (!p || !o) return fail(CP_EINVAL, "null argument");
+  o->chunks_total = p->st.n_chunks();
+  o->chunks_used = p->st.chunks_used();
+  o->pages_used = p->st.pages_used();
+  o->pages_reserved = p->st.pages_reserved();
+  o->requests_open = p->st.n_open();
+  o->models = p->st.n_models();
+  return CP_OK;
+}
+
+cp_status cp_model_register(cp_pool *p, const cp_model_desc *m, int32_t *model_id) {
+  if (!p || !m || !model_id) return fail(CP_EINVAL, "null argument");
+  if (m->dtype != CP_BF16) return fail(CP_EINVAL, "only bf16 KV is supported");
+  Geom g;
+  g.kind = m->kind;
+  g.hq = m->n_q_heads;
+  g.hkv = m->n_kv_heads;
+  g.head_dim = m->head_dim;
+  g.latent = m->latent_dim;
+  g.rope = m->rope_dim;
+  g.scale = m->softmax_scale;
+  std::string e = p->st.add_model(g, model_id);
+  if (!e.empty()) return fail(CP_EINVAL, "%s", e.c_str());
+  return CP_OK;
+}
+
+cp_status cp_model_info(cp_pool *p, int32_t id, cp_model_info_t *o) {
+  if (!p || !o) return fail(CP_EINVAL, "null argument");
+  if (id < 0 || id >= p->st.n_models()) return fail(CP_EINVAL, "unknown model id %d", id);
+  const Geom &g = p->st.model(id);
+  o->d_k = g.d_k;
+  o->d_v = g.d_v;
+  o->kappa = g.kappa;
+  o->page_bytes = (int32_t)g.page_bytes;
+  o->pages_per_chunk = g.ppc;
+  o->row_elems = g.row_elems;
+  return CP_OK;
+}
+
+cp_status cp_request_open(cp_pool *p, int32_t model_id, int64_t reserve_tokens, int32_t *req_id) {
+  if (!p || !req_id) return fail(CP_EINVAL, "null argument");
+  std::string err;
+  int rc = p->st.open(model_id, reserve_tokens, req_id, &err);
+  if (rc == -3) return fail(CP_ENOSPC, "%s", err.c_str());
+  if (rc != 0) return fail(CP_EINVAL, "%s", err.c_str());
+  return CP_OK;
+}
+
+cp_status cp_request_close(cp_pool *p, int32_t req_id) {
+  if (!p) return fail(CP_EINVAL, "null pool");
+  if (!p->st.valid_open(req_id)) return fail(CP_EINVAL, "request %d is not open", req_id);
+  p->st.close(req_id);
+  return CP_OK;
+}
+
+cp_status cp_request_len(cp_pool *p, int32_t req_id, int64_t *ctx_len) {
+  if (!p || !ctx_len) return fail(CP_EINVAL, "null argument");
+  if (!p->st.valid_open(req_id)) return fail(CP_EINVAL, "request %d is not open", req_id);
+  *ctx_len = p->st.req(req_id).ctx_len;
+  return CP_OK;
+}
+
+cp_status cp_request_pages(cp_pool *p, int32_t req_id, int64_t first, int64_t count, uint32_t *ptes) {
+  if (!p || (!ptes && count > 0)) return fail(CP_EINVAL, "null argument");
+  if (!p->st.valid_open(req_id)) return fail(CP_EINVAL, "request %d is not open", req_id);
+  const Request &r = p->st.req(req_id);
+  if (first < 0 || count < 0 || first + count > r.pages_used)
+    return fail(CP_EINVAL, "page range [%lld, %lld) outside the %lld used pages", (long long)first,
+                (long long)(first + count), (long long)r.pages_used);
+  std::memcpy(ptes, p->st.pte_mirror() + r.pte_base + first, (size_t)count * 4);
+  return CP_OK;
+}
+
+}  // extern "C"
+
+namespace {
+
+// Fills the kernel view of a model's geometry. `variant` selects the code
+// path (set by the caller for decode).
+GeomK geom_k(const Geom &g, int32_t P) {
+  GeomK k{};
+  k.kind = g.kind;
+  k.hq = g.hq;
+  k.hkv = g.hkv;
+  k.g = g.g;
+  k.d_k = g.d_k;
+  k.d_v = g.d_v;
+  k.row_elems = g.row_elems;
+  k.page_tokens = P;
+  k.page_bytes = (int32_t)g.page_bytes;
+  k.scale_log2 = g.scale * 1.4426950408889634f;
+  k.variant = 0;
+  k.nb = 1;
+  return k;
+}
+
+cp_status check_ids(cp_pool *p, int32_t n, const int32_t *ids) {
+  if (n < 0) return fail(CP_EINVAL, "negative request count");
+  if (n > 0 && !ids) return fail(CP_EINVAL, "null req_ids");
+  std::vector<int32_t> s(ids, ids + n);
+  for (int32_t i = 0; i < n; ++i)
+    if (!p->st.valid_open(s[i])) return fail(CP_EINVAL, "request %d is not open", s[i]);
+  std::sort(s.begin(), s.end());
+  for (int32_t i = 1; i < n; ++i)
+    if (s[i] == s[i - 1]) return fail(CP_EINVAL, "request %d appears twice in one call", s[i]);
+  return CP_OK;
+}
+
+// Copies page-table entries [lo, hi) to the device through the pinned copy.
+cp_status push_ptes(cp_pool *p, uint64_t lo, uint64_t hi, hipStream_t s) {
+  if (hi <= lo) return CP_OK;
+  std::memcpy(p->pin_pte + lo, p->st.pte_mirror() + lo, (size_t)(hi - lo) * 4);
+  hipError_t e = hipMemcpyAsync(p->dev_pte + lo, p->pin_pte + lo, (size_t)(hi - lo) * 4, hipMemcpyHostToDevice, s);
+  if (e != hipSuccess) return hip_fail(e, "page-table copy");
+  return CP_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+cp_status cp_kv_append(cp_pool *p, int32_t n, const int32_t *req_ids, const int32_t *n_new, const void *rows,
+                       void *hip_stream) {
+  if (!p) return fail(CP_EINVAL, "null pool");
+  cp_status rc = check_ids(p, n, req_ids);
+  if (rc) return rc;
+  if (n > 0 && !n_new) return fail(CP_EINVAL, "null n_new");
+  int64_t total = 0;
+  for (int32_t i = 0; i < n; ++i) {
+    if (n_new[i] < 0) return fail(CP_EINVAL, "negative n_new for request %d", req_ids[i]);
+    const Request &r = p->st.req(req_ids[i]);
+    int64_t nl = r.ctx_len + n_new[i];
+    if (nl > 0xFFFFFFF0ll) return fail(CP_EINVAL, "context length overflow");
+    if (!p->st.fits_reservation(req_ids[i], nl))
+      return fail(CP_EINVAL, "request %d would grow to %lld tokens, past its reservation of %lld pages", req_ids[i],
+                  (long long)nl, (long long)r.reserve_pages);
+    total += n_new[i];
+  }
+  if (p->host_only) {
+    if (rows) return fail(CP_EINVAL, "host-only pool: rows must be NULL");
+  } else if (total > 0 && !rows) {
+    return fail(CP_EINVAL, "null rows");
+  }
+  if (total == 0) return CP_OK;
+  if (total > 0x7FFFFFFF) return fail(CP_EINVAL, "too many rows in one call");
+
+  // All checks passed: allocate pages and update host page tables.
+  std::vector<uint32_t> old_len(n);
+  uint64_t lo = UINT64_MAX, hi = 0;
+  for (int32_t i = 0; i < n; ++i) {
+    const Request &r = p->st.req(req_ids[i]);
+    old_len[i] = (uint32_t)r.ctx_len;
+    uint64_t first, count;
+    p->st.grow(req_ids[i], r.ctx_len + n_new[i], &first, &count);
+    if (count) {
+      lo = std::min(lo, first);
+      hi = std::max(hi, first + count);
+    }
+  }
+  if (p->host_only) return CP_OK;
+
+  DeviceGuard g(p->device);
+  hipStream_t s = (hipStream_t)hip_stream;
+  rc = push_ptes(p, lo, hi, s);
+  if (rc) return rc;
+
+  // Launch groups of at most kMaxReqPerLaunch requests and kMaxLaunchModels models.
+  const int32_t P = p->st.page_tokens();
+  uint64_t src = 0;  // element offset of the current request's rows
+  int32_t i = 0;
+  while (i < n) {
+    AppendArgs a{};
+    a.pool = p->dev_pool;
+    a.pte = p->dev_pte;
+    a.rows = (const uint16_t *)rows;
+    int32_t nm = 0, model_map[16];
+    for (int k = 0; k < 16; ++k) model_map[k] = -1;
+    uint32_t grid_rows = 0;
+    while (i < n && a.n_req < kMaxReqPerLaunch) {
+      const Request &r = p->st.req(req_ids[i]);
+      int32_t mi = model_map[r.model];
+      if (mi < 0) {
+        if (nm == kMaxLaunchModels) break;
+        mi = model_map[r.model] = nm;
+        a.geom[nm++] = geom_k(p->st.model(r.model), P);
+      }
+      const Geom &gm = p->st.model(r.model);
+      if (n_new[i] > 0) {
+        AppReq &q = a.req[a.n_req++];
+        q.src_off = src;
+        q.row_begin = grid_rows;
+        q.n_new = (uint32_t)n_new[i];
+        q.old_len = old_len[i];
+        q.pte_base = r.pte_base;
+        q.model = (uint32_t)mi;
+        grid_rows += (uint32_t)n_new[i];
+      }
+      src += (uint64_t)n_new[i] * (uint64_t)gm.row_elems;
+      ++i;
+    }
+    a.total_rows = (int32_t)grid_rows;
+    if (a.n_req > 0) {
+      hipError_t e = launch_append(a, s);
+      if (e != hipSuccess) return hip_fail(e, "append launch");
+    }
+  }
+  return CP_OK;
+}
+
+cp_status cp_kv_gather(cp_pool *p, int32_t req_id, int64_t start, int64_t n_tok, void *dst, void *hip_stream) {
+  if (!p) return fail(CP_EINVAL, "null pool");
+  if (p->host_only) return fail(CP_ESTATE, "host-only pool has no device data");
+  if (!p->st.valid_open(req_id)) return fail(CP_EINVAL, "request %d is not open", req_id);
+  const Request &r = p->st.req(req_id);
+  if (start < 0 || n_tok < 0 || start + n_tok > r.ctx_len)
+    return fail(CP_EINVAL, "range [%lld, %lld) outside the context of %lld tokens", (long long)start,
+                (long long)(start + n_tok), (long long)r.ctx_len);
+  if (n_tok == 0) return CP_OK;
+  if (!dst) return fail(CP_EINVAL, "null dst");
+  DeviceGuard g(p->device);
+  GatherArgs a{};
+  a.pool = p->dev_pool;
+  a.pte = p->dev_pte;
+  a.dst = (uint16_t *)dst;
+  a.pte_base = r.pte_base;
+  a.start = (uint32_t)start;
+  a.n_tok = (uint32_t)n_tok;
+  a.geom = geom_k(p->st.model(r.model), p->st.page_tokens());
+  hipError_t e = launch_gather(a, (hipStream_t)hip_stream);
+  if (e != hipSuccess) return hip_fail(e, "gather launch");
+  return CP_OK;
+}
+
+}  // extern "C"
+
+namespace {
+
+// Vector-path variant for a model: heads per block and V values per lane.
+void choose_valu(const Geom &g, GeomK *k) {
+  const int hb = g.g > 8 ? 16 : 8;
+  const int dpl = g.d_v / 64;
+  int v = 0;
+  switch (dpl) {
+    case 8: v = 0; break;
+    case 4: v = 1; break;
+    case 2: v = 2; break;
+    default: v = 3; break;
+  }
+  k->variant = v + (hb == 8 ? 4 : 0);
+  k->nb = (g.g + hb - 1) / hb;
+}
+
+cp_status ensure_ws(cp_pool *p, uint64_t o_floats, uint64_t l_floats) {
+  if (o_floats <= p->ws_o_cap && l_floats <= p->ws_l_cap) return CP_OK;
+  // Growth is rare; wait for in-flight users of the old workspace.
+  if (hipDeviceSynchronize() != hipSuccess) return fail(CP_EHIP, "synchronise before workspace growth");
+  if (o_floats > p->ws_o_cap) {
+    uint64_t cap = std::max<uint64_t>(o_floats, p->ws_o_cap * 2);
+    if (p->ws_o) (void)hipFree(p->ws_o);
+    p->ws_o = nullptr;
+    p->ws_o_cap = 0;
+    if (hipMalloc((void **)&p->ws_o, cap * 4) != hipSuccess) return fail(CP_ENOMEM, "workspace allocation failed");
+    p->ws_o_cap = cap;
+  }
+  if (l_floats > p->ws_l_cap) {
+    uint64_t cap = std::max<uint64_t>(l_floats, p->ws_l_cap * 2);
+    if (p->ws_l) (void)hipFree(p->ws_l);
+    p->ws_l = nullptr;
+    p->ws_l_cap = 0;
+    if (hipMalloc((void **)&p->ws_l, cap * 4) != hipSuccess) return fail(CP_ENOMEM, "workspace allocation failed");
+    p->ws_l_cap = cap;
+  }
+  return CP_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+cp_status cp_attn_decode_ex(cp_pool *p, int32_t n, const int32_t *req_ids, const void *q, void *out, float *lse,
+                            void *hip_stream, const cp_decode_opts *opts) {
+  if (!p) return fail(CP_EINVAL, "null pool");
+  if (p->host_only) return fail(CP_ESTATE, "host-only pool cannot decode");
+  if (n < 1) return fail(CP_EINVAL, "decode needs at least one request");
+  cp_status rc = check_ids(p, n, req_ids);
+  if (rc) return rc;
+  if (!q || !out || !lse) return fail(CP_EINVAL, "null q, out or lse");
+  cp_decode_opts o{};
+  o.persistent = 1;
+  if (opts) o = *opts;
+  if (o.num_splits < 0) return fail(CP_EINVAL, "num_splits must be >= 0");
+  if (o.path < CP_PATH_AUTO || o.path > CP_PATH_MFMA) return fail(CP_EINVAL, "unknown path %d", o.path);
+  const int32_t P = p->st.page_tokens();
+  for (int32_t i = 0; i < n; ++i) {
+    const Request &r = p->st.req(req_ids[i]);
+    if (r.ctx_len < 1) return fail(CP_EINVAL, "request %d has an empty context", req_ids[i]);
+  }
+
+  // Per-model kernel geometry and head blocking.
+  std::vector<GeomK> gk(p->st.n_models());
+  for (int32_t m = 0; m < p->st.n_models(); ++m) {
+    gk[m] = geom_k(p->st.model(m), P);
+    choose_valu(p->st.model(m), &gk[m]);
+  }
+
+  // Packed offsets in call order.
+  std::vector<uint64_t> q_off(n), o_off(n), l_off(n);
+  uint64_t qo = 0, oo = 0, lo = 0;
+  std::vector<PlanIn> pin(n);
+  std::vector<int32_t> hblk(n);
+  for (int32_t i = 0; i < n; ++i) {
+    const Request &r = p->st.req(req_ids[i]);
+    const Geom &g = p->st.model(r.model);
+    q_off[i] = qo;
+    o_off[i] = oo;
+    l_off[i] = lo;
+    qo += (uint64_t)g.hq * g.d_k;
+    oo += (uint64_t)g.hq * g.d_v;
+    lo += (uint64_t)g.hq;
+    pin[i] = PlanIn{r.model, r.ctx_len};
+    hblk[i] = g.hkv * gk[r.model].nb;
+  }
+  if (qo > 0xFFFFFFFFull || oo > 0xFFFFFFFFull) return fail(CP_EINVAL, "batch too large");
+
+  std::vector<PlanReq> plan;
+  plan_splits(pin, [&] {
+    std::vector<Geom> v;
+    for (int32_t m = 0; m < p->st.n_models(); ++m) v.push_back(p->st.model(m));
+    return v;
+  }(), P, (int64_t)p->num_cus * 2, 1, o.num_splits, hblk, &plan);
+  for (auto &pr : plan)
+    if (pr.chunk_pages > 0xFFFF || pr.n_chunks > 0xFFFF) return fail(CP_EINVAL, "context too long to split");
+
+  // Work order: costliest units first (stable in call order).
+  std::vector<int32_t> order(n);
+  for (int32_t i = 0; i < n; ++i) order[i] = i;
+  std::stable_sort(order.begin(), order.end(), [&](int32_t x, int32_t y) {
+    const Geom &gx = p->st.model(p->st.req(req_ids[x]).model);
+    const Geom &gy = p->st.model(p->st.req(req_ids[y]).model);
+    return (double)plan[x].chunk_pages * gx.page_bytes > (double)plan[y].chunk_pages * gy.page_bytes;
+  });
+
+  // Workspace for split requests.
+  uint64_t ws_rows = 0, ws_floats = 0;
+  std::vector<uint32_t> ws_base(n, kNoWs), ws_orow(n, 0);
+  for (int32_t i = 0; i < n; ++i) {
+    if (plan[i].n_chunks <= 1) continue;
+    const Geom &g = p->st.model(p->st.req(req_ids[i]).model);
+    ws_base[i] = (uint32_t)ws_rows;
+    ws_rows += (uint64_t)plan[i].n_chunks * g.hq;
+    ws_floats = (ws_floats + 511) / 512 * 512;
+    ws_orow[i] = (uint32_t)(ws_floats / (uint64_t)g.d_v);
+    ws_floats += (uint64_t)plan[i].n_chunks * g.hq * g.d_v;
+  }
+  if (ws_rows >= kNoWs || ws_floats / 64 >= kNoWs) return fail(CP_EINVAL, "split workspace too large");
+
+  DeviceGuard dg(p->device);
+  hipStream_t s = (hipStream_t)hip_stream;
+  if (ws_rows) {
+    rc = ensure_ws(p, ws_floats, ws_rows);
+    if (rc) return rc;
+  }
+
+  if (o.ev_begin) {
+    hipError_t e = hipEventRecord((hipEvent_t)o.ev_begin, s);
+    if (e != hipSuccess) return hip_fail(e, "event record");
+  }
+  // Decode launches in groups.
+  int32_t idx = 0;
+  while (idx < n) {
+    DecodeArgs a{};
+    a.pool = p->dev_pool;
+    a.pte = p->dev_pte;
+    a.q = (const uint16_t *)q;
+    a.out = (uint16_t *)out;
+    a.lse = lse;
+    a.ws_o = p->ws_o;
+    a.ws_l = p->ws_l;
+    a.queue = p->queue;
+    int32_t nm = 0, model_map[16];
+    for (int k = 0; k < 16; ++k) model_map[k] = -1;
+    uint32_t units = 0;
+    while (idx < n && a.n_req < kMaxReqPerLaunch) {
+      const int32_t i = order[idx];
+      const Request &r = p->st.req(req_ids[i]);
+      int32_t mi = model_map[r.model];
+      if (mi < 0) {
+        if (nm == kMaxLaunchModels) break;
+        mi = model_map[r.model] = nm;
+        a.geom[nm++] = gk[r.model];
+      }
+      DecReq &d = a.req[a.n_req++];
+      d.pte_base = r.pte_base;
+      d.ctx_len = (uint32_t)r.ctx_len;
+      d.q_off = (uint32_t)q_off[i];
+      d.o_off = (uint32_t)o_off[i];
+      d.lse_off = (uint32_t)l_off[i];
+      d.ws_base = ws_base[i];
+      d.ws_orow = ws_orow[i];
+      d.unit_begin = units;
+      d.chunk_pages = (uint16_t)plan[i].chunk_pages;
+      d.n_chunks = (uint16_t)plan[i].n_chunks;
+      d.model = (uint8_t)mi;
+      d.n_hblk = (uint16_t)plan[i].n_hblk;
+      units += (uint32_t)plan[i].n_chunks * (uint32_t)plan[i].n_hblk;
+      ++idx;
+    }
+    a.n_units = (int32_t)units;
+    a.persistent = o.persistent ? 1 : 0;
+    int grid = (int)units;
+    if (a.persistent) grid = (int)std::min<uint32_t>(units, (uint32_t)p->num_cus * 2);
+    hipError_t e = launch_decode_valu(a, grid, s);
+    if (e != hipSuccess) return hip_fail(e, "decode launch");
+  }
+  if (o.ev_end) {
+    hipError_t e = hipEventRecord((hipEvent_t)o.ev_end, s);
+    if (e != hipSuccess) return hip_fail(e, "event record");
+  }
+
+  // Merge launches for split requests.
+  MergeArgs ma{};
+  ma.ws_o = p->ws_o;
+  ma.ws_l = p->ws_l;
+  ma.out = (uint16_t *)out;
+  ma.lse = lse;
+  auto flush = [&]() -> cp_status {
+    if (ma.n_req == 0) return CP_OK;
+    hipError_t e = launch_merge(ma, s);
+    if (e != hipSuccess) return hip_fail(e, "merge launch");
+    ma.n_req = 0;
+    ma.total_heads = 0;
+    return CP_OK;
+  };
+  for (int32_t i = 0; i < n; ++i) {
+    if (ws_base[i] == kNoWs) continue;
+    if (ma.n_req == kMaxReqPerLaunch) {
+      rc = flush();
+      if (rc) return rc;
+    }
+    const Geom &g = p->st.model(p->st.req(req_ids[i]).model);
+    MergeReq &m = ma.req[ma.n_req++];
+    m.head_begin = (uint32_t)ma.total_heads;
+    m.hq = (uint32_t)g.hq;
+    m.d_v = (uint32_t)g.d_v;
+    m.n_chunks = (uint32_t)plan[i].n_chunks;
+    m.ws_base = ws_base[i];
+    m.ws_orow = ws_orow[i];
+    m.o_off = (uint32_t)o_off[i];
+    m.lse_off = (uint32_t)l_off[i];
+    ma.total_heads += g.hq;
+  }
+  return flush();
+}
+
+cp_status cp_attn_decode(cp_pool *p, int32_t n, const int32_t *req_ids, const void *q, void *out, float *lse,
+                         void *hip_stream) {
+  return cp_attn_decode_ex(p, n, req_ids, q, out, lse, hip_stream, nullptr);
+}
+
+}  // extern "C"

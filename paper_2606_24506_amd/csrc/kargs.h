@@ -1,0 +1,102 @@
+// Kernel-argument records shared by the host launcher (api.cpp) and the
+// kernels (kernels.hip). Everything a launch needs travels by value in the
+// kernel-argument segment, so a decode step costs no host-to-device copy.
+// Sizes stay well under the 4 KiB argument limit.
+#pragma once
+#include <stdint.h>
+
+namespace cp {
+
+constexpr int kMaxLaunchModels = 4;   // distinct models in one decode launch
+constexpr int kMaxReqPerLaunch = 64;  // requests in one launch
+constexpr uint32_t kNoWs = 0xFFFFFFFFu;
+
+// Per-model geometry as the kernels see it.
+struct GeomK {
+  int32_t kind;        // 0 MLA, 1 GQA
+  int32_t hq, hkv, g;  // g = hq / hkv
+  int32_t d_k, d_v, row_elems, page_tokens;
+  int32_t page_bytes;
+  int32_t variant;     // kernel code path chosen by the host
+  float scale_log2;    // softmax scale * log2(e)
+  int32_t nb;          // head blocks per KV head (vector path)
+};
+
+// One request of a decode launch.
+struct DecReq {
+  uint32_t pte_base;  // first page-table entry of the request
+  uint32_t ctx_len;   // tokens to attend over (>= 1)
+  uint32_t q_off;     // bf16 element offset of the request's queries
+  uint32_t o_off;     // bf16 element offset of its outputs
+  uint32_t lse_off;   // float offset of its log-sum-exp values
+  uint32_t ws_base;   // first partial lse row (kNoWs when the request is not split)
+  uint32_t ws_orow;   // partial outputs start at float offset ws_orow * d_v
+  uint32_t unit_begin;
+  uint16_t chunk_pages;  // pages per KV range
+  uint16_t n_chunks;     // KV ranges
+  uint8_t model;         // index into DecodeArgs::geom
+  uint8_t pad;
+  uint16_t n_hblk;       // head blocks per KV range
+};
+
+struct DecodeArgs {
+  const uint8_t *pool;
+  const uint32_t *pte;
+  const uint16_t *q;
+  uint16_t *out;
+  float *lse;
+  float *ws_o;        // partial outputs, [row][d_v] fp32, normalised
+  float *ws_l;        // partial log-sum-exp, [row], natural log
+  uint32_t *queue;    // persistent mode: {next unit, finished workgroups}
+  int32_t n_req, n_units, persistent, pad;
+  GeomK geom[kMaxLaunchModels];
+  DecReq req[kMaxReqPerLaunch];
+};
+
+struct MergeReq {
+  uint32_t head_begin;  // first merge row of this request in the grid
+  uint32_t hq, d_v, n_chunks;
+  uint32_t ws_base, ws_orow, o_off, lse_off;
+};
+
+struct MergeArgs {
+  const float *ws_o;
+  const float *ws_l;
+  uint16_t *out;
+  float *lse;
+  int32_t n_req, total_heads, pad0, pad1;
+  MergeReq req[kMaxReqPerLaunch];
+};
+
+struct AppReq {
+  uint64_t src_off;    // bf16 element offset of the request's first row in the input
+  uint32_t row_begin;  // first grid row of this request in the launch
+  uint32_t n_new;
+  uint32_t old_len;
+  uint32_t pte_base;
+  uint32_t model;
+  uint32_t pad;
+};
+
+struct AppendArgs {
+  uint8_t *pool;
+  const uint32_t *pte;
+  const uint16_t *rows;
+  int32_t n_req, total_rows, pad0, pad1;
+  GeomK geom[kMaxLaunchModels];
+  AppReq req[kMaxReqPerLaunch];
+};
+
+struct GatherArgs {
+  const uint8_t *pool;
+  const uint32_t *pte;
+  uint16_t *dst;
+  uint32_t pte_base, start, n_tok, pad;
+  GeomK geom;
+};
+
+static_assert(sizeof(DecodeArgs) <= 3072, "decode kernel arguments too large");
+static_assert(sizeof(MergeArgs) <= 3072, "merge kernel arguments too large");
+static_assert(sizeof(AppendArgs) <= 3072, "append kernel arguments too large");
+
+}  // namespace cp

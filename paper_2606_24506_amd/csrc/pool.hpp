@@ -1,0 +1,172 @@
+// Host-side bookkeeping of the shared KV pool: model geometry, the chunk
+// and page allocator, admission against the page budget, per-request page
+// tables, and the split-KV work planner. Plain C++17, no HIP: the device
+// side lives in api.cpp and kernels.hip.
+//
+// Terms. The pool budget is n_chunks chunks of chunk_bytes. A chunk is
+// carved into pages of one model at a time (a per-model slab), so models
+// with different per-token bytes kappa(M) share one budget without mixing
+// page sizes inside a chunk (Section 3.1: one pool page budget across
+// heterogeneous models; Section 2.3 C1). A page holds page_tokens tokens.
+// A page-table entry (PTE) is the page's byte offset in the pool >> 8.
+#pragma once
+
+#include <cstdint>
+#include <map>
+#include <queue>
+#include <string>
+#include <vector>
+
+namespace cp {
+
+enum Kind : int32_t { kMLA = 0, kGQA = 1 };
+
+struct Geom {
+  int32_t kind = 0;
+  int32_t hq = 0, hkv = 0, g = 0;  // g = query heads per KV head
+  int32_t head_dim = 0, latent = 0, rope = 0;
+  int32_t d_k = 0, d_v = 0;
+  int32_t row_elems = 0;  // bf16 elements of one logical row
+  int32_t kappa = 0;      // bytes per token
+  int64_t page_bytes = 0;
+  int32_t ppc = 0;        // pages per chunk
+  float scale = 0.f;
+};
+
+struct Request {
+  bool open = false;
+  int32_t model = -1;
+  int64_t ctx_len = 0;
+  int64_t reserve_pages = 0;
+  int64_t pages_used = 0;
+  uint32_t pte_base = 0;
+};
+
+// Deterministic 64-bit generator (splitmix64), used for seeded placement.
+struct SplitMix64 {
+  uint64_t s;
+  explicit SplitMix64(uint64_t seed = 0) : s(seed) {}
+  uint64_t next() {
+    uint64_t z = (s += 0x9E3779B97F4A7C15ull);
+    z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+    z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+    return z ^ (z >> 31);
+  }
+};
+
+// First-fit allocator of contiguous ranges in [0, capacity), with coalescing.
+class RangeAlloc {
+ public:
+  void init(uint64_t capacity);
+  bool alloc(uint64_t len, uint64_t *start);
+  void release(uint64_t start, uint64_t len);
+  uint64_t capacity() const { return cap_; }
+
+ private:
+  uint64_t cap_ = 0;
+  std::map<uint64_t, uint64_t> free_;  // start -> len
+};
+
+class PoolState {
+ public:
+  // Returns "" on success, or an error message.
+  std::string init(int32_t page_tokens, uint64_t pool_bytes, uint64_t chunk_bytes, uint64_t seed,
+                   int32_t max_requests);
+
+  int32_t page_tokens() const { return P_; }
+  uint64_t chunk_bytes() const { return chunk_bytes_; }
+  uint64_t n_chunks() const { return n_chunks_; }
+  uint64_t pte_capacity() const { return pte_.size(); }
+  uint64_t pool_bytes_used() const { return n_chunks_ * chunk_bytes_; }
+
+  // Models.
+  std::string add_model(const Geom &g_in, int32_t *id);
+  int32_t n_models() const { return (int32_t)models_.size(); }
+  const Geom &model(int32_t i) const { return models_[i]; }
+
+  // Requests.
+  int32_t max_requests() const { return (int32_t)reqs_.size(); }
+  bool valid_open(int32_t id) const { return id >= 0 && id < (int32_t)reqs_.size() && reqs_[id].open; }
+  const Request &req(int32_t id) const { return reqs_[id]; }
+  // Admission (returns 0, or -3 for budget exhausted, -1 for bad args).
+  int open(int32_t model, int64_t reserve_tokens, int32_t *id, std::string *err);
+  void close(int32_t id);
+  int32_t n_open() const { return n_open_; }
+
+  // Would growing these requests to the given lengths stay within their
+  // reservations? (checked before any state change)
+  bool fits_reservation(int32_t id, int64_t new_len) const;
+  // Allocate the pages needed to grow request id to new_len tokens and
+  // record them in the PTE mirror. Returns the index range of PTEs written
+  // as [*first, *first + *count). Never fails for admitted requests within
+  // their reservation.
+  void grow(int32_t id, int64_t new_len, uint64_t *first, uint64_t *count);
+
+  const uint32_t *pte_mirror() const { return pte_.data(); }
+  uint32_t *pte_mirror_mut() { return pte_.data(); }
+
+  // Accounting.
+  uint64_t chunks_used() const { return n_chunks_ - free_count(); }
+  uint64_t pages_used() const;
+  uint64_t pages_reserved() const;
+  // Chunks the budget must hold if every open reservation were filled.
+  uint64_t committed_chunks(int32_t extra_model, int64_t extra_pages) const;
+
+ private:
+  struct Chunk {
+    int32_t model = -1;
+    int32_t used = 0;
+    std::vector<uint64_t> bits;  // free-slot bitmap while carved
+  };
+  struct ModelAcct {
+    int64_t reserved = 0;   // pages promised to open requests
+    int64_t used = 0;       // pages holding KV
+    int64_t held = 0;       // chunks carved for this model
+    std::map<int32_t, int32_t> partial;  // chunk -> free slots (chunks with room)
+  };
+
+  uint64_t free_count() const { return seed_ ? free_rand_.size() : free_heap_.size(); }
+  int32_t take_chunk();
+  void give_chunk(int32_t c);
+  uint32_t alloc_page(int32_t model);
+  void free_page(uint32_t pte);
+
+  int32_t P_ = 64;
+  uint64_t chunk_bytes_ = 0, n_chunks_ = 0, seed_ = 0;
+  SplitMix64 rng_;
+  std::vector<Chunk> chunks_;
+  std::priority_queue<int32_t, std::vector<int32_t>, std::greater<int32_t>> free_heap_;
+  std::vector<int32_t> free_rand_;
+  std::vector<Geom> models_;
+  std::vector<ModelAcct> acct_;
+  std::vector<Request> reqs_;
+  std::vector<int32_t> free_ids_;
+  int32_t n_open_ = 0;
+  std::vector<uint32_t> pte_;
+  RangeAlloc pte_ranges_;
+};
+
+// ---------------------------------------------------------------- planner
+
+// One request of a decode call as the planner sees it.
+struct PlanIn {
+  int32_t model;
+  int64_t ctx_len;
+};
+
+struct PlanReq {
+  int32_t n_chunks = 1;     // KV ranges (splits)
+  int32_t chunk_pages = 1;  // pages per range (last may be shorter)
+  int32_t n_hblk = 1;       // head blocks per range
+};
+
+// Split rule. Every request's pages are cut into page-aligned ranges so the
+// whole batch yields about target_units work units of similar byte cost,
+// and never fewer pages per range than min_pages. force_splits > 0 gives
+// each request min(force_splits, pages) ranges. The result depends only on
+// the batch's models and lengths, never on page placement.
+void plan_splits(const std::vector<PlanIn> &in, const std::vector<Geom> &models, int32_t page_tokens,
+                 int64_t target_units, int32_t min_pages, int32_t force_splits, const std::vector<int32_t> &hblk,
+                 std::vector<PlanReq> *out);
+
+}  // namespace cp

@@ -1,0 +1,249 @@
+"""C-ABI library on the CPU: it loads, exports every declared symbol, and its
+host-side bookkeeping (admission against the page budget, page allocation,
+page-table entries, placement) behaves as documented. A host-only pool
+(device = -1) runs all of this without a GPU."""
+import math
+import os
+import re
+import subprocess
+
+import numpy as np
+import pytest
+
+from paper_2606_24506_amd import crosspool as cpl
+from workloads import MODELS
+
+HDR = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "crosspool.h")
+MLA16, MQA32, GQA = MODELS["mla16"], MODELS["mqa32"], MODELS["gqa32x4"]
+
+
+def declared_functions():
+    text = open(HDR).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(cp_[a-z_0-9]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_function():
+    names = declared_functions()
+    assert len(names) >= 14
+    for n in names:
+        assert hasattr(cpl.LIB, n), n
+    out = subprocess.run(["nm", "-D", "--defined-only", cpl._LIB_PATH], capture_output=True, text=True).stdout
+    exported = set(re.findall(r"\bT (cp_[a-z_0-9]+)", out))
+    assert set(names) <= exported, set(names) - exported
+
+
+def host_pool(pool_bytes=64 << 20, chunk=2 << 20, seed=0, max_requests=0):
+    return cpl.Pool(page_tokens=64, pool_bytes=pool_bytes, chunk_bytes=chunk, placement_seed=seed, device=-1,
+                    max_requests=max_requests)
+
+
+def reg_all(p):
+    return p.register_spec(MLA16), p.register_spec(MQA32), p.register_spec(GQA)
+
+
+def test_model_geometry():
+    p = host_pool()
+    a, b, c = reg_all(p)
+    ia, ib, ic = p.info(a), p.info(b), p.info(c)
+    assert (ia["kappa"], ia["page_bytes"], ia["pages_per_chunk"], ia["d_k"], ia["d_v"]) == (1152, 73728, 28, 576, 512)
+    assert (ib["kappa"], ib["page_bytes"], ib["pages_per_chunk"]) == (512, 32768, 64)
+    assert (ic["kappa"], ic["page_bytes"], ic["pages_per_chunk"], ic["row_elems"]) == (2048, 131072, 16, 1024)
+    p.destroy()
+
+
+@pytest.mark.parametrize("kw,msg", [
+    (dict(kind=cpl.CP_KIND_MLA, n_q_heads=16, n_kv_heads=2, latent_dim=512, rope_dim=64, softmax_scale=0.1), "exactly one"),
+    (dict(kind=cpl.CP_KIND_MLA, n_q_heads=16, n_kv_heads=1, latent_dim=512, rope_dim=64), "softmax_scale"),
+    (dict(kind=cpl.CP_KIND_GQA, n_q_heads=30, n_kv_heads=4, head_dim=128), "divide"),
+    (dict(kind=cpl.CP_KIND_GQA, n_q_heads=32, n_kv_heads=4, head_dim=96), "V width"),
+    (dict(kind=cpl.CP_KIND_GQA, n_q_heads=512, n_kv_heads=4, head_dim=128), "n_q_heads"),
+    (dict(kind=7, n_q_heads=8, n_kv_heads=1, head_dim=128), "kind"),
+])
+def test_model_register_rejects_bad_geometry(kw, msg):
+    p = host_pool()
+    with pytest.raises(cpl.CrossPoolError) as e:
+        cpl.cp_model_register(p.handle, **kw)
+    assert e.value.status == cpl.CP_EINVAL and msg in e.value.message
+    p.destroy()
+
+
+def test_pool_create_validation():
+    with pytest.raises(cpl.CrossPoolError):
+        cpl.cp_pool_create(page_tokens=0, pool_bytes=1 << 20, device=-1)
+    with pytest.raises(cpl.CrossPoolError):
+        cpl.cp_pool_create(page_tokens=64, pool_bytes=1 << 20, chunk_bytes=2 << 20, device=-1)  # < one chunk
+    with pytest.raises(cpl.CrossPoolError):
+        cpl.cp_pool_create(page_tokens=64, pool_bytes=1 << 30, chunk_bytes=1000, device=-1)
+
+
+def pte_to_chunk_slot(pte, chunk, page_bytes):
+    off = int(pte) << 8
+    return off // chunk, (off % chunk) // page_bytes, (off % chunk) % page_bytes
+
+
+def test_page_tables_and_placement():
+    chunk = 2 << 20
+    p = host_pool(pool_bytes=64 * chunk, chunk=chunk, seed=0)
+    a, b, c = reg_all(p)
+    ra = p.open(a, 5000)
+    rb = p.open(b, 3000)
+    rc = p.open(c, 1000)
+    p.append([ra, rb, rc], [4000, 3000, 1000], None)
+    assert [p.ctx_len(r) for r in (ra, rb, rc)] == [4000, 3000, 1000]
+    seen = {}
+    for r, mid in ((ra, a), (rb, b), (rc, c)):
+        pb = p.info(mid)["page_bytes"]
+        ptes = p.pages(r)
+        assert len(ptes) == math.ceil(p.ctx_len(r) / 64)
+        for e in ptes:
+            ch, slot, rem = pte_to_chunk_slot(e, chunk, pb)
+            assert rem == 0 and ch < 64 and slot < chunk // pb
+            assert seen.setdefault(ch, mid) == mid, "a chunk holds pages of one model only"
+            assert (ch, slot) not in seen.get("slots", set())
+            seen.setdefault("slots", set()).add((ch, slot))
+    # seed 0: chunks handed out in ascending order, slots filled in order
+    first = p.pages(ra)[:3]
+    assert [pte_to_chunk_slot(e, chunk, 73728)[:2] for e in first] == [(0, 0), (0, 1), (0, 2)]
+    for r in (ra, rb, rc):
+        p.close(r)
+    s = p.stats()
+    assert s["chunks_used"] == 0 and s["pages_used"] == 0 and s["pages_reserved"] == 0 and s["requests_open"] == 0
+    p.destroy()
+
+
+def placement(seed):
+    p = host_pool(pool_bytes=256 << 20, seed=seed)
+    a, b, c = reg_all(p)
+    rs = [p.open(a, 20000), p.open(c, 9000)]
+    for _ in range(5):
+        p.append(rs, [3000, 1500], None)
+    out = [p.pages(r).copy() for r in rs]
+    for r in rs:
+        p.close(r)
+    p.destroy()
+    return out
+
+
+def test_seeded_placement_is_reproducible_and_scattered():
+    x1, x2, y = placement(7), placement(7), placement(8)
+    assert all(np.array_equal(u, v) for u, v in zip(x1, x2))
+    assert not all(np.array_equal(u, v) for u, v in zip(x1, y))
+    chunks = np.array(x1[0], dtype=np.uint64) * 256 // (2 << 20)
+    assert len(np.unique(chunks)) > 1 and not np.all(np.diff(chunks.astype(np.int64)) >= 0)
+
+
+def test_admission_reject_changes_nothing():
+    chunk = 2 << 20
+    p = host_pool(pool_bytes=10 * chunk, chunk=chunk)
+    a, b, c = reg_all(p)
+    r1 = p.open(a, 64 * 28 * 6)  # six MLA chunks
+    r2 = p.open(c, 64 * 16 * 3)  # three GQA chunks
+    before = p.stats()
+    with pytest.raises(cpl.CrossPoolError) as e:
+        p.open(b, 64 * 64 * 2)  # two MQA chunks do not fit in the one left
+    assert e.value.status == cpl.CP_ENOSPC
+    assert p.stats() == before
+    r3 = p.open(b, 64 * 64)  # exactly one chunk fits
+    # admitted requests always get their pages, up to the reservation
+    p.append([r1, r2, r3], [64 * 28 * 6, 64 * 16 * 3, 64 * 64], None)
+    s = p.stats()
+    assert s["chunks_used"] == 10 and s["pages_used"] == 28 * 6 + 16 * 3 + 64
+    with pytest.raises(cpl.CrossPoolError) as e:
+        p.open(a, 1)
+    assert e.value.status == cpl.CP_ENOSPC
+    p.close(r2)
+    r4 = p.open(a, 64 * 28 * 3)
+    p.append([r4], [64 * 28 * 3], None)
+    for r in (r1, r3, r4):
+        p.close(r)
+    p.destroy()
+
+
+def test_append_errors_are_atomic():
+    p = host_pool()
+    a, b, c = reg_all(p)
+    r1, r2 = p.open(a, 100), p.open(b, 100)
+    p.append([r1, r2], [10, 10], None)
+    before = (p.stats(), p.ctx_len(r1), p.ctx_len(r2))
+    for ids, nn in (([r1, r2], [10, 91]),  # past r2's reservation (2 pages = 128 tokens ok; 101 ok) -> use 200
+                    ([r1, r1], [1, 1]), ([r1, 999], [1, 1]), ([r1], [-1])):
+        if nn == [10, 91]:
+            nn = [10, 200]
+        with pytest.raises(cpl.CrossPoolError) as e:
+            p.append(ids, nn, None)
+        assert e.value.status == cpl.CP_EINVAL
+        assert (p.stats(), p.ctx_len(r1), p.ctx_len(r2)) == before
+    p.append([r1], [118], None)  # fills the reservation exactly (2 pages = 128 tokens)
+    with pytest.raises(cpl.CrossPoolError):
+        p.append([r1], [1], None)
+    with pytest.raises(cpl.CrossPoolError) as e:
+        p.decode([r1], 0, 0, 0)
+    assert e.value.status == cpl.CP_ESTATE
+    with pytest.raises(cpl.CrossPoolError) as e:
+        p.gather(r1, 0, 1, 0)
+    assert e.value.status == cpl.CP_ESTATE
+    p.close(r1)
+    with pytest.raises(cpl.CrossPoolError) as e:
+        p.close(r1)
+    assert e.value.status == cpl.CP_EINVAL
+    with pytest.raises(cpl.CrossPoolError) as e:
+        p.destroy()  # r2 still open
+    assert e.value.status == cpl.CP_ESTATE
+    p.close(r2)
+    p.destroy()
+
+
+def test_request_table_limit():
+    p = host_pool(max_requests=3)
+    a, _, _ = reg_all(p)
+    ids = [p.open(a, 64) for _ in range(3)]
+    with pytest.raises(cpl.CrossPoolError) as e:
+        p.open(a, 64)
+    assert e.value.status == cpl.CP_ENOSPC
+    for r in ids:
+        p.close(r)
+    p.destroy()
+
+
+def test_random_admission_never_strands_admitted_requests():
+    """Random open / append / close traffic over three models. Whatever was
+    admitted can always be filled to its full reservation, rejections change
+    nothing, and pages are conserved."""
+    rng = np.random.default_rng(123)
+    chunk = 2 << 20
+    p = host_pool(pool_bytes=24 * chunk, chunk=chunk, seed=99)
+    mids = reg_all(p)
+    live = {}
+    for step in range(600):
+        op = rng.integers(0, 3)
+        if op == 0 or not live:
+            m = int(rng.integers(0, 3))
+            res = int(rng.integers(1, 6000))
+            before = p.stats()
+            try:
+                r = p.open(mids[m], res)
+                live[r] = res
+            except cpl.CrossPoolError as e:
+                assert e.status == cpl.CP_ENOSPC and p.stats() == before
+        elif op == 1:
+            r = int(rng.choice(list(live)))
+            room = live[r] - p.ctx_len(r)
+            if room > 0:
+                p.append([r], [int(rng.integers(1, room + 1))], None)
+        else:
+            r = int(rng.choice(list(live)))
+            p.close(r)
+            del live[r]
+        s = p.stats()
+        assert s["chunks_used"] <= s["chunks_total"]
+        assert s["pages_used"] == sum(math.ceil(p.ctx_len(r) / 64) for r in live)
+    # fill every admitted request completely
+    for r, res in live.items():
+        room = res - p.ctx_len(r)
+        if room:
+            p.append([r], [room], None)
+    for r in list(live):
+        p.close(r)
+    assert p.stats()["chunks_used"] == 0
+    p.destroy()
