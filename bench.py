@@ -76,7 +76,6 @@ def cpu_baseline(wl, budget_s: float):
         oracle.decode(rows, wl.q_bits[r], wl.model(r))
         t_total += time.perf_counter() - t0
         done.append(r)
-        nbytes += algorithmic_bytes_decode(wl, [0] * 0) if False else 0
         if t_total >= budget_s:
             break
     from workloads import algorithmic_bytes

@@ -17,7 +17,9 @@
 namespace cp {
 hipError_t launch_append(const AppendArgs &a, hipStream_t stream);
 hipError_t launch_gather(const GatherArgs &a, hipStream_t stream);
-hipError_t launch_decode_valu(const DecodeArgs &a, int grid, hipStream_t stream);
+hipError_t launch_decode(const DecodeArgs &a, int grid, uint32_t mask, hipStream_t stream);
+int decode_waves(int variant);
+int decode_wgs_per_cu(uint32_t mask);
 hipError_t launch_merge(const MergeArgs &a, hipStream_t stream);
 }  // namespace cp
 
@@ -402,6 +404,29 @@ void choose_valu(const Geom &g, GeomK *k) {
   k->nb = (g.g + hb - 1) / hb;
 }
 
+constexpr int32_t kMatrixFirst = 16;
+
+// Matrix-core variant for a model, or -1 when none fits its geometry. The
+// matrix path is used where at least 16 query heads share one KV head, so
+// the per-KV-head work is a dense contraction (MLA latent head, MQA, wide
+// GQA groups); it needs page_tokens to be a multiple of 32.
+int32_t matrix_variant(const Geom &g, int32_t P) {
+  if (P % 32) return -1;
+  if (g.kind == kMLA && g.latent == 512 && g.rope == 64) {
+    if (g.g == 16) return 16;
+    if (g.g == 32) return 17;
+    if (g.g == 128) return 18;
+    return -1;
+  }
+  if (g.kind == kGQA && g.head_dim == 128) {
+    if (g.g == 16) return 19;
+    if (g.g == 32) return 20;
+    if (g.g == 64) return 21;
+    if (g.g == 128) return 22;
+  }
+  return -1;
+}
+
 cp_status ensure_ws(cp_pool *p, uint64_t o_floats, uint64_t l_floats) {
   if (o_floats <= p->ws_o_cap && l_floats <= p->ws_l_cap) return CP_OK;
   // Growth is rare; wait for in-flight users of the old workspace.
@@ -448,11 +473,23 @@ cp_status cp_attn_decode_ex(cp_pool *p, int32_t n, const int32_t *req_ids, const
     if (r.ctx_len < 1) return fail(CP_EINVAL, "request %d has an empty context", req_ids[i]);
   }
 
-  // Per-model kernel geometry and head blocking.
+  // Per-model kernel variant and head blocking.
   std::vector<GeomK> gk(p->st.n_models());
   for (int32_t m = 0; m < p->st.n_models(); ++m) {
-    gk[m] = geom_k(p->st.model(m), P);
-    choose_valu(p->st.model(m), &gk[m]);
+    const Geom &g = p->st.model(m);
+    gk[m] = geom_k(g, P);
+    const int32_t mv = o.path == CP_PATH_VALU ? -1 : matrix_variant(g, P);
+    if (mv >= 0) {
+      gk[m].variant = mv;
+      gk[m].nb = 1;
+    } else {
+      choose_valu(g, &gk[m]);
+    }
+  }
+  for (int32_t i = 0; i < n; ++i) {
+    const int32_t m = p->st.req(req_ids[i]).model;
+    if (o.path == CP_PATH_MFMA && gk[m].variant < kMatrixFirst)
+      return fail(CP_EINVAL, "model %d has no matrix-core variant (needs >= 16 query heads per KV head)", m);
   }
 
   // Packed offsets in call order.
@@ -474,19 +511,33 @@ cp_status cp_attn_decode_ex(cp_pool *p, int32_t n, const int32_t *req_ids, const
   }
   if (qo > 0xFFFFFFFFull || oo > 0xFFFFFFFFull) return fail(CP_EINVAL, "batch too large");
 
+  // Work units: about two per CU, or one per CU when every request takes
+  // the 128-head matrix path (its per-unit partials are large); at least
+  // four pages per range so the four waves of a workgroup all get pages.
+  bool all_wide = true, any_matrix = false;
+  for (int32_t i = 0; i < n; ++i) {
+    const int32_t v = gk[p->st.req(req_ids[i]).model].variant;
+    all_wide = all_wide && (v == 18 || v == 22);
+    any_matrix = any_matrix || v >= kMatrixFirst;
+  }
   std::vector<PlanReq> plan;
   plan_splits(pin, [&] {
     std::vector<Geom> v;
     for (int32_t m = 0; m < p->st.n_models(); ++m) v.push_back(p->st.model(m));
     return v;
-  }(), P, (int64_t)p->num_cus * 2, 1, o.num_splits, hblk, &plan);
+  }(), P, (int64_t)p->num_cus * (all_wide ? 1 : 2), any_matrix ? 4 : 1, o.num_splits, hblk, &plan);
   for (auto &pr : plan)
     if (pr.chunk_pages > 0xFFFF || pr.n_chunks > 0xFFFF) return fail(CP_EINVAL, "context too long to split");
 
-  // Work order: costliest units first (stable in call order).
+  // Work order: requests whose kernels use the same workgroup size launch
+  // together; inside a launch the costliest units go first (stable in call
+  // order).
+  auto wclass = [&](int32_t i) { return decode_waves(gk[p->st.req(req_ids[i]).model].variant); };
   std::vector<int32_t> order(n);
   for (int32_t i = 0; i < n; ++i) order[i] = i;
   std::stable_sort(order.begin(), order.end(), [&](int32_t x, int32_t y) {
+    const int cx = wclass(x), cy = wclass(y);
+    if (cx != cy) return cx < cy;
     const Geom &gx = p->st.model(p->st.req(req_ids[x]).model);
     const Geom &gy = p->st.model(p->st.req(req_ids[y]).model);
     return (double)plan[x].chunk_pages * gx.page_bytes > (double)plan[y].chunk_pages * gy.page_bytes;
@@ -532,7 +583,8 @@ cp_status cp_attn_decode_ex(cp_pool *p, int32_t n, const int32_t *req_ids, const
     int32_t nm = 0, model_map[16];
     for (int k = 0; k < 16; ++k) model_map[k] = -1;
     uint32_t units = 0;
-    while (idx < n && a.n_req < kMaxReqPerLaunch) {
+    const int cls = wclass(order[idx]);
+    while (idx < n && a.n_req < kMaxReqPerLaunch && wclass(order[idx]) == cls) {
       const int32_t i = order[idx];
       const Request &r = p->st.req(req_ids[i]);
       int32_t mi = model_map[r.model];
@@ -559,9 +611,12 @@ cp_status cp_attn_decode_ex(cp_pool *p, int32_t n, const int32_t *req_ids, const
     }
     a.n_units = (int32_t)units;
     a.persistent = o.persistent ? 1 : 0;
+    uint32_t mask = 0;
+    for (int32_t k = 0; k < nm; ++k) mask |= 1u << a.geom[k].variant;
     int grid = (int)units;
-    if (a.persistent) grid = (int)std::min<uint32_t>(units, (uint32_t)p->num_cus * 2);
-    hipError_t e = launch_decode_valu(a, grid, s);
+    if (a.persistent)
+      grid = (int)std::min<uint32_t>(units, (uint32_t)p->num_cus * (uint32_t)decode_wgs_per_cu(mask));
+    hipError_t e = launch_decode(a, grid, mask, s);
     if (e != hipSuccess) return hip_fail(e, "decode launch");
   }
   if (o.ev_end) {

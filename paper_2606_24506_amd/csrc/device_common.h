@@ -1,0 +1,59 @@
+// Device helpers shared by the gfx950 kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "kargs.h"
+
+namespace cp {
+
+#define CP_DEV __device__ __forceinline__
+
+CP_DEV float bf16_to_f32(uint32_t b) { return __uint_as_float(b << 16); }
+
+// Round to nearest even; quiet NaN stays NaN.
+CP_DEV uint32_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return 0x7fc0u;
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return u >> 16;
+}
+
+CP_DEV float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+CP_DEV float fast_log2(float x) { return __builtin_amdgcn_logf(x); }
+
+constexpr float kLn2 = 0.693147180559945309f;
+
+CP_DEV float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+
+CP_DEV float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+CP_DEV const uint8_t *page_ptr(const uint8_t *pool, const uint32_t *pte, uint32_t pte_base, uint32_t page) {
+  return pool + ((uint64_t)pte[pte_base + page] << 8);
+}
+
+// Byte offset, inside a page, of 16-byte segment `seg` of the logical row of
+// token slot `slot` (row = [K heads | V heads] for GQA, [latent | rope] for MLA).
+CP_DEV uint64_t row_seg_offset(const GeomK &g, uint32_t slot, uint32_t seg) {
+  const uint32_t e = seg * 8;  // first bf16 element of the segment
+  if (g.kind == 0) return (uint64_t)slot * (uint32_t)(g.d_k * 2) + (uint64_t)e * 2;
+  const uint32_t d = (uint32_t)g.d_k, hk = (uint32_t)g.hkv, P = (uint32_t)g.page_tokens;
+  const uint64_t head_blk = (uint64_t)2 * P * d * 2;
+  if (e < hk * d) {
+    const uint32_t kh = e / d, off = e - kh * d;
+    return kh * head_blk + (uint64_t)slot * d * 2 + (uint64_t)off * 2;
+  }
+  const uint32_t e2 = e - hk * d, kh = e2 / d, off = e2 - kh * d;
+  return kh * head_blk + (uint64_t)P * d * 2 + (uint64_t)slot * d * 2 + (uint64_t)off * 2;
+}
+
+}  // namespace cp

@@ -9,57 +9,11 @@
 // A page starts at pool + (pte << 8).
 #include <hip/hip_runtime.h>
 
+#include "decode_mfma.h"
+#include "device_common.h"
 #include "kargs.h"
 
 namespace cp {
-
-#define CP_DEV __device__ __forceinline__
-
-CP_DEV float bf16_to_f32(uint32_t b) { return __uint_as_float(b << 16); }
-
-// Round to nearest even; quiet NaN stays NaN.
-CP_DEV uint32_t f32_to_bf16(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return 0x7fc0u;
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return u >> 16;
-}
-
-CP_DEV float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
-CP_DEV float fast_log2(float x) { return __builtin_amdgcn_logf(x); }
-
-constexpr float kLn2 = 0.693147180559945309f;
-
-CP_DEV float wave_max(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
-  return v;
-}
-
-CP_DEV float wave_sum(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
-  return v;
-}
-
-CP_DEV const uint8_t *page_ptr(const uint8_t *pool, const uint32_t *pte, uint32_t pte_base, uint32_t page) {
-  return pool + ((uint64_t)pte[pte_base + page] << 8);
-}
-
-// Byte offset, inside a page, of 16-byte segment `seg` of the logical row of
-// token slot `slot` (row = [K heads | V heads] for GQA, [latent | rope] for MLA).
-CP_DEV uint64_t row_seg_offset(const GeomK &g, uint32_t slot, uint32_t seg) {
-  const uint32_t e = seg * 8;  // first bf16 element of the segment
-  if (g.kind == 0) return (uint64_t)slot * (uint32_t)(g.d_k * 2) + (uint64_t)e * 2;
-  const uint32_t d = (uint32_t)g.d_k, hk = (uint32_t)g.hkv, P = (uint32_t)g.page_tokens;
-  const uint64_t head_blk = (uint64_t)2 * P * d * 2;
-  if (e < hk * d) {
-    const uint32_t kh = e / d, off = e - kh * d;
-    return kh * head_blk + (uint64_t)slot * d * 2 + (uint64_t)off * 2;
-  }
-  const uint32_t e2 = e - hk * d, kh = e2 / d, off = e2 - kh * d;
-  return kh * head_blk + (uint64_t)P * d * 2 + (uint64_t)slot * d * 2 + (uint64_t)off * 2;
-}
 
 // ------------------------------------------------------------- append
 
@@ -144,7 +98,7 @@ constexpr int kLdsFloats = 16 * 1024 + 4 * 2 * 16 + 64;
 // its own online-softmax state; the four states are combined at the end in
 // a fixed order. Scores live in the log2 domain: s2 = scale*log2(e)*<q, k>.
 template <int HB, int DPL>
-__device__ void valu_unit(const DecodeArgs &a, const GeomK &gm, const DecReq &rq, uint32_t chunk, uint32_t hblk,
+__device__ __forceinline__ void valu_unit(const DecodeArgs &a, const GeomK &gm, const DecReq &rq, uint32_t chunk, uint32_t hblk,
                           float *lds) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int P = gm.page_tokens;
@@ -295,44 +249,97 @@ __device__ void valu_unit(const DecodeArgs &a, const GeomK &gm, const DecReq &rq
   __syncthreads();  // LDS is reused by the next unit
 }
 
-// Vector-path variants: (heads per block, V elements per lane).
-enum : int32_t { kV16x8 = 0, kV16x4, kV16x2, kV16x1, kV8x8, kV8x4, kV8x2, kV8x1 };
+// Code-path variants (GeomK::variant). Vector path (ids 0-7): heads per
+// block and V elements per lane. Matrix path (ids 16-22): head blocks per
+// wave, waves per tile, waves per workgroup, K width, V width, tile tokens.
+enum : int32_t {
+  kV16x8 = 0, kV16x4, kV16x2, kV16x1, kV8x8, kV8x4, kV8x2, kV8x1,
+  kM_MLA_G16 = 16, kM_MLA_G32, kM_MLA_G128, kM_D128_G16, kM_D128_G32, kM_D128_G64, kM_D128_G128
+};
 
-__device__ void run_unit(const DecodeArgs &a, uint32_t u, float *lds) {
+template <int V> struct Mcfg;
+template <> struct Mcfg<kM_MLA_G16> { using C = MfmaCfg<1, 1, 4, 576, 512, 16, true>; };
+template <> struct Mcfg<kM_MLA_G32> { using C = MfmaCfg<1, 2, 2, 576, 512, 16, true>; };
+template <> struct Mcfg<kM_MLA_G128> { using C = MfmaCfg<1, 8, 8, 576, 512, 32, true>; };
+template <> struct Mcfg<kM_D128_G16> { using C = MfmaCfg<1, 1, 4, 128, 128, 32, false>; };
+template <> struct Mcfg<kM_D128_G32> { using C = MfmaCfg<2, 1, 4, 128, 128, 32, false>; };
+template <> struct Mcfg<kM_D128_G64> { using C = MfmaCfg<4, 1, 4, 128, 128, 32, false>; };
+template <> struct Mcfg<kM_D128_G128> { using C = MfmaCfg<2, 4, 4, 128, 128, 32, false>; };
+
+// Waves per workgroup of each variant (vector variants use four).
+constexpr int variant_waves(int v) {
+  return v == kM_MLA_G32 ? 2 : v == kM_MLA_G128 ? 8 : 4;
+}
+
+template <int V>
+constexpr int mcfg_buf() { return Mcfg<V>::C::BUF; }
+
+constexpr bool has(uint32_t mask, int v) { return (mask >> v) & 1u; }
+
+// LDS bytes of one KV buffer for a kernel covering the variant set `mask`.
+constexpr int kernel_buf_bytes(uint32_t mask) {
+  int b = 0;
+  if (mask & 0xFFu) b = kLdsFloats * 4 > b ? kLdsFloats * 4 : b;
+#define CP_B(V) if (has(mask, V) && mcfg_buf<V>() > b) b = mcfg_buf<V>();
+  CP_B(kM_MLA_G16) CP_B(kM_MLA_G32) CP_B(kM_MLA_G128) CP_B(kM_D128_G16) CP_B(kM_D128_G32) CP_B(kM_D128_G64)
+  CP_B(kM_D128_G128)
+#undef CP_B
+  return b;
+}
+
+template <uint32_t MASK>
+__device__ __forceinline__ void run_unit(const DecodeArgs &a, uint32_t u, char *buf0, char *buf1, float *red) {
   int r = 0;
   while (r + 1 < a.n_req && a.req[r + 1].unit_begin <= u) ++r;
   const DecReq &rq = a.req[r];
   const GeomK &gm = a.geom[rq.model];
   const uint32_t local = u - rq.unit_begin;
   const uint32_t chunk = local / rq.n_hblk, hblk = local % rq.n_hblk;
-  switch (gm.variant) {
-    case kV16x8: valu_unit<16, 8>(a, gm, rq, chunk, hblk, lds); break;
-    case kV16x4: valu_unit<16, 4>(a, gm, rq, chunk, hblk, lds); break;
-    case kV16x2: valu_unit<16, 2>(a, gm, rq, chunk, hblk, lds); break;
-    case kV16x1: valu_unit<16, 1>(a, gm, rq, chunk, hblk, lds); break;
-    case kV8x8: valu_unit<8, 8>(a, gm, rq, chunk, hblk, lds); break;
-    case kV8x4: valu_unit<8, 4>(a, gm, rq, chunk, hblk, lds); break;
-    case kV8x2: valu_unit<8, 2>(a, gm, rq, chunk, hblk, lds); break;
-    default: valu_unit<8, 1>(a, gm, rq, chunk, hblk, lds); break;
+  float *lds = reinterpret_cast<float *>(buf0);
+#define CP_VCASE(V, HB, DPL)                                        \
+  if constexpr (has(MASK, V)) {                                     \
+    if (gm.variant == V) {                                          \
+      valu_unit<HB, DPL>(a, gm, rq, chunk, hblk, lds);              \
+      return;                                                       \
+    }                                                               \
   }
+  CP_VCASE(kV16x8, 16, 8) CP_VCASE(kV16x4, 16, 4) CP_VCASE(kV16x2, 16, 2) CP_VCASE(kV16x1, 16, 1)
+  CP_VCASE(kV8x8, 8, 8) CP_VCASE(kV8x4, 8, 4) CP_VCASE(kV8x2, 8, 2) CP_VCASE(kV8x1, 8, 1)
+#undef CP_VCASE
+#define CP_MCASE(V, HBW, WPT, NW, DK, DV, T, MLA)                                    \
+  if constexpr (has(MASK, V)) {                                                      \
+    if (gm.variant == V) {                                                           \
+      mfma_unit<HBW, WPT, NW, DK, DV, T, MLA>(a, gm, rq, chunk, hblk, buf0, buf1, red); \
+      return;                                                                        \
+    }                                                                                \
+  }
+  CP_MCASE(kM_MLA_G16, 1, 1, 4, 576, 512, 16, true)
+  CP_MCASE(kM_MLA_G32, 1, 2, 2, 576, 512, 16, true)
+  CP_MCASE(kM_MLA_G128, 1, 8, 8, 576, 512, 32, true)
+  CP_MCASE(kM_D128_G16, 1, 1, 4, 128, 128, 32, false)
+  CP_MCASE(kM_D128_G32, 2, 1, 4, 128, 128, 32, false)
+  CP_MCASE(kM_D128_G64, 4, 1, 4, 128, 128, 32, false)
+  CP_MCASE(kM_D128_G128, 2, 4, 4, 128, 128, 32, false)
+#undef CP_MCASE
 }
 
-__global__ __launch_bounds__(256) void decode_valu_kernel(const DecodeArgs a) {
-  __shared__ float lds[kLdsFloats];
-  __shared__ uint32_t next;
+// Work loop shared by the decode kernels. Persistent mode: workgroups pull
+// unit indices from a device counter until the queue is empty; the last
+// workgroup to leave resets the counters for the next launch.
+template <uint32_t MASK>
+__device__ __forceinline__ void decode_loop(const DecodeArgs &a, char *buf0, char *buf1, float *red, uint32_t *next) {
   if (!a.persistent) {
-    run_unit(a, blockIdx.x, lds);
+    run_unit<MASK>(a, blockIdx.x, buf0, buf1, red);
     return;
   }
   for (;;) {
-    if (threadIdx.x == 0) next = atomicAdd(&a.queue[0], 1u);
+    if (threadIdx.x == 0) *next = atomicAdd(&a.queue[0], 1u);
     __syncthreads();
-    const uint32_t u = next;
+    const uint32_t u = *next;
     __syncthreads();
     if (u >= (uint32_t)a.n_units) break;
-    run_unit(a, u, lds);
+    run_unit<MASK>(a, u, buf0, buf1, red);
   }
-  // The last workgroup to finish resets the queue for the next launch.
   if (threadIdx.x == 0) {
     __threadfence();
     if (atomicAdd(&a.queue[1], 1u) == gridDim.x - 1) {
@@ -342,9 +349,72 @@ __global__ __launch_bounds__(256) void decode_valu_kernel(const DecodeArgs a) {
   }
 }
 
-hipError_t launch_decode_valu(const DecodeArgs &a, int grid, hipStream_t stream) {
-  hipLaunchKernelGGL(decode_valu_kernel, dim3(grid), dim3(256), 0, stream, a);
-  return hipGetLastError();
+// One kernel per variant set; NW waves per workgroup, two KV buffers sized
+// for the largest variant in the set.
+template <uint32_t MASK, int NW>
+__global__ __launch_bounds__(64 * NW) void decode_kernel(const DecodeArgs a) {
+  constexpr int B = kernel_buf_bytes(MASK);
+  __shared__ __attribute__((aligned(16))) char buf0[B];
+  __shared__ __attribute__((aligned(16))) char buf1[(MASK >> 16) ? B : 16];
+  __shared__ float red[kRedFloats];
+  __shared__ uint32_t next;
+  decode_loop<MASK>(a, buf0, buf1, red, &next);
+}
+
+constexpr uint32_t vbit(int v) { return 1u << v; }
+// The variant sets the host launches together: each single variant, and
+// the mixed MLA-16 / MQA-32 / GQA-8 batch.
+constexpr uint32_t kMixedSmall = vbit(kV8x2) | vbit(kM_MLA_G16) | vbit(kM_D128_G32);
+constexpr uint32_t kAll4 = 0xFFu | vbit(kM_MLA_G16) | vbit(kM_D128_G16) | vbit(kM_D128_G32) | vbit(kM_D128_G64) |
+                           vbit(kM_D128_G128);
+
+// Picks the kernel instantiation that covers `mask`. Returns
+// hipErrorInvalidValue for a set no instantiation covers (the host keeps
+// variants of different workgroup sizes in separate launches).
+hipError_t launch_decode(const DecodeArgs &a, int grid, uint32_t mask, hipStream_t stream) {
+  const dim3 g(grid);
+#define CP_L(M, NW)                                                                   \
+  case M:                                                                             \
+    hipLaunchKernelGGL((decode_kernel<M, NW>), g, dim3(64 * NW), 0, stream, a);       \
+    return hipGetLastError();
+  switch (mask) {
+    CP_L(vbit(kV16x8), 4) CP_L(vbit(kV16x4), 4) CP_L(vbit(kV16x2), 4) CP_L(vbit(kV16x1), 4)
+    CP_L(vbit(kV8x8), 4) CP_L(vbit(kV8x4), 4) CP_L(vbit(kV8x2), 4) CP_L(vbit(kV8x1), 4)
+    CP_L(vbit(kM_MLA_G16), 4) CP_L(vbit(kM_MLA_G32), 2) CP_L(vbit(kM_MLA_G128), 8)
+    CP_L(vbit(kM_D128_G16), 4) CP_L(vbit(kM_D128_G32), 4) CP_L(vbit(kM_D128_G64), 4) CP_L(vbit(kM_D128_G128), 4)
+    CP_L(kMixedSmall, 4)
+    default: break;
+  }
+#undef CP_L
+  if ((mask & ~kAll4) == 0) {
+    hipLaunchKernelGGL((decode_kernel<kAll4, 4>), g, dim3(256), 0, stream, a);
+    return hipGetLastError();
+  }
+  return hipErrorInvalidValue;
+}
+
+int decode_waves(int variant) { return variant_waves(variant); }
+
+// Workgroups of one kernel that fit on a CU at once (LDS-bound).
+int decode_wgs_per_cu(uint32_t mask) {
+  int b = 0;
+  for (int v = 0; v < 32; ++v) {
+    if (!((mask >> v) & 1u)) continue;
+    int bytes = 0;
+    switch (v) {
+      case kM_MLA_G16: bytes = 2 * mcfg_buf<kM_MLA_G16>(); break;
+      case kM_MLA_G32: bytes = 2 * mcfg_buf<kM_MLA_G32>(); break;
+      case kM_MLA_G128: bytes = 2 * mcfg_buf<kM_MLA_G128>(); break;
+      case kM_D128_G16: bytes = 2 * mcfg_buf<kM_D128_G16>(); break;
+      case kM_D128_G32: bytes = 2 * mcfg_buf<kM_D128_G32>(); break;
+      case kM_D128_G64: bytes = 2 * mcfg_buf<kM_D128_G64>(); break;
+      case kM_D128_G128: bytes = 2 * mcfg_buf<kM_D128_G128>(); break;
+      default: bytes = kLdsFloats * 4; break;
+    }
+    b = bytes > b ? bytes : b;
+  }
+  const int per = (160 * 1024) / (b + 4 * kRedFloats + 64);
+  return per < 1 ? 1 : per;
 }
 
 // ------------------------------------------------------------- merge

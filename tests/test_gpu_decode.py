@@ -115,15 +115,50 @@ def test_ragged_mixed_batch(splits, path):
         ld.close()
 
 
+VARIANT_MODELS = [("mla16", 700), ("mla32", 333), ("mla128", 290), ("mqa16", 515), ("mqa32", 190),
+                  ("gqa128x2", 257), ("mqa128", 129), ("gqa32x4", 450), ("gqa8x8d64", 97)]
+
+
+@pytest.mark.parametrize("splits", [0, 1, 5])
+@pytest.mark.parametrize("persistent", [1, 0])
+def test_every_kernel_variant(splits, persistent):
+    """One request per geometry, so every matrix-core and vector variant runs
+    (workgroups of 2, 4 and 8 waves in separate launches of one call)."""
+    wl = custom(VARIANT_MODELS, seed=41)
+    ld = load(wl, interleave=31)
+    try:
+        ld.decode(num_splits=splits, persistent=persistent)
+        torch.cuda.synchronize()
+        compare(ld, {r: expected_for(wl, r) for r in range(len(VARIANT_MODELS))}, f"variants s{splits} p{persistent}")
+        # the vector path on the same data agrees too
+        ld.decode(num_splits=splits, persistent=persistent, path=cpl.CP_PATH_VALU)
+        torch.cuda.synchronize()
+        compare(ld, {r: expected_for(wl, r) for r in range(len(VARIANT_MODELS))}, f"variants vector s{splits}")
+    finally:
+        ld.close()
+
+
+def test_forced_matrix_path_rejects_narrow_groups():
+    wl = custom([("gqa32x4", 10)], seed=3)
+    ld = load(wl)
+    try:
+        with pytest.raises(cpl.CrossPoolError) as e:
+            ld.decode(path=cpl.CP_PATH_MFMA)
+        assert e.value.status == cpl.CP_EINVAL
+    finally:
+        ld.close()
+
+
 def test_single_token_returns_v_exactly():
     """n = 1: the softmax weight is exactly 1, so every head's output is its
     KV head's V row, bit for bit, and lse is the scaled score."""
-    wl = custom([("mla16", 1), ("mqa32", 1), ("gqa32x4", 1), ("mla128", 1), ("mla16", 40)], seed=9)
+    wl = custom([("mla16", 1), ("mqa32", 1), ("gqa32x4", 1), ("mla128", 1), ("mla32", 1), ("mqa128", 1),
+                 ("mla16", 40)], seed=9)
     ld = load(wl)
     try:
         ld.decode()
         torch.cuda.synchronize()
-        for r in range(4):
+        for r in range(6):
             m = wl.model(r)
             row = wl.rows_bits(r)[0]
             got = ld.out_bits(r)
@@ -135,7 +170,7 @@ def test_single_token_returns_v_exactly():
                     d = m.head_dim
                     v = row[m.n_kv_heads * d + kv * d: m.n_kv_heads * d + (kv + 1) * d]
                 assert np.array_equal(got[h], v), f"request {r} head {h}"
-        compare(ld, {r: expected_for(wl, r) for r in range(5)}, "single-token")
+        compare(ld, {r: expected_for(wl, r) for r in range(7)}, "single-token")
     finally:
         ld.close()
 

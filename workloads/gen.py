@@ -69,6 +69,12 @@ MODELS: Dict[str, ModelSpec] = {
     "mla128": ModelSpec("mla128", "mla", 128, 1, latent_dim=512, rope_dim=64, scale=1.0 / math.sqrt(192.0)),
     "mqa32": ModelSpec("mqa32", "gqa", 32, 1, head_dim=128, scale=1.0 / math.sqrt(128.0)),
     "gqa32x4": ModelSpec("gqa32x4", "gqa", 32, 4, head_dim=128, scale=1.0 / math.sqrt(128.0)),
+    # Further geometries, used to exercise every kernel variant in tests.
+    "mla32": ModelSpec("mla32", "mla", 32, 1, latent_dim=512, rope_dim=64, scale=1.0 / math.sqrt(192.0)),
+    "mqa16": ModelSpec("mqa16", "gqa", 16, 1, head_dim=128, scale=1.0 / math.sqrt(128.0)),
+    "gqa128x2": ModelSpec("gqa128x2", "gqa", 128, 2, head_dim=128, scale=1.0 / math.sqrt(128.0)),
+    "mqa128": ModelSpec("mqa128", "gqa", 128, 1, head_dim=128, scale=1.0 / math.sqrt(128.0)),
+    "gqa8x8d64": ModelSpec("gqa8x8d64", "gqa", 8, 8, head_dim=64, scale=1.0 / math.sqrt(64.0)),
 }
 
 
