@@ -46,9 +46,12 @@ def parse():
     ap.add_argument("--config", type=int, default=2, choices=[1, 2, 3, 4, 5])
     ap.add_argument("--layers", type=int, default=0, help="KV copies cycled by the steps (0: enough to exceed 1 GiB)")
     ap.add_argument("--path", type=int, default=0, help="0 auto, 1 vector, 2 matrix cores")
-    ap.add_argument("--splits", type=int, default=0)
+    ap.add_argument("--splits", type=int, default=0, help="forced KV ranges per request (queue/grid schedules)")
+    ap.add_argument("--schedule", type=int, default=0, help="0 balanced, 1 work queue, 2 one workgroup per unit")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="target CPU time of the oracle sample")
+    ap.add_argument("--copy-mib", type=int, default=0,
+                    help="before timing, run one device copy of this many MiB (reference for HBM byte counters)")
     return ap.parse_args()
 
 
@@ -143,7 +146,7 @@ def main():
     def step(i, evs=None):
         ld = lds[i % layers]
         ld.pool.append(ld.req_ids, ones, new_rows, stream)
-        opts = dict(num_splits=args.splits, path=args.path)
+        opts = dict(num_splits=args.splits, path=args.path, schedule=args.schedule)
         if evs is not None:
             opts.update(ev_begin=evs[0].cuda_event, ev_end=evs[1].cuda_event)
         ld.pool.decode(ld.req_ids, ld.q, ld.out, ld.lse, stream, **opts)
@@ -161,10 +164,16 @@ def main():
         visits[li] += 1
         dec_bytes += algorithmic_bytes_decode(wl, ctx)
         app_bytes += sum(2 * wl.model(r).kappa + 4 for r in range(B))
+    if args.copy_mib:
+        src = torch.empty(args.copy_mib << 20, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        del src, dst
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
         step(args.warmup + i, ev[i])
+    t_enq = time.perf_counter() - t0
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     kern_ms = sum(a.elapsed_time(b) for a, b in ev) / args.steps
@@ -193,8 +202,10 @@ def main():
             "layers_cycled": layers,
             "step": "cp_kv_append (1 token/request) + cp_attn_decode",
             "path": ["auto", "vector", "matrix"][args.path],
+            "schedule": ["balanced", "queue", "grid"][args.schedule],
         },
         "req_tokens_per_s": round(B / (wall / args.steps), 1),
+        "host_enqueue_ms_per_step": round(t_enq * 1e3 / args.steps, 5),
         "context_tokens_per_s": round(sum(ctx0[0]) / (wall / args.steps), 1),
         "roofline": {
             "bound": "hbm",

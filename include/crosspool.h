@@ -227,18 +227,30 @@ typedef enum {
   CP_PATH_MFMA = 2  /* force the matrix-core kernel for every model */
 } cp_path;
 
+typedef enum {
+  /* Persistent grid, one workgroup per CU slot; the launch's pages, in
+   * request order, are cut into equal-cost contiguous ranges, one per
+   * workgroup, so ragged contexts and mixed models balance to within one
+   * page. A request spanning several ranges is merged afterwards. */
+  CP_SCHED_BALANCED = 0,
+  /* Persistent grid whose workgroups pull (request, KV range) units from a
+   * device queue, costliest first. */
+  CP_SCHED_QUEUE = 1,
+  /* One workgroup per (request, KV range) unit. */
+  CP_SCHED_GRID = 2
+} cp_schedule;
+
 typedef struct {
-  /* 0: the planner chooses the split of each request's context into KV
-   * ranges; k >= 1 forces min(k, pages) page-aligned ranges per request. */
+  /* Queue and grid schedules: 0 lets the planner split each request's
+   * context into page-aligned KV ranges; k >= 1 forces min(k, pages)
+   * ranges per request. Must be 0 with the balanced schedule. */
   int32_t num_splits;
-  /* 1 (default when opts == NULL): a persistent grid pulls work units from
-   * a device queue, longest first; 0: one workgroup per unit. */
-  int32_t persistent;
-  /* cp_path */
-  int32_t path;
+  int32_t schedule; /* cp_schedule; opts == NULL means CP_SCHED_BALANCED */
+  int32_t path;     /* cp_path */
   int32_t reserved0;
   /* Optional hipEvent_t handles recorded on the stream immediately before
-   * and after the main attention kernel (not the merge), for timing. */
+   * the first and after the last attention kernel of the call (the split
+   * merge is not included), for timing. */
   void *ev_begin;
   void *ev_end;
 } cp_decode_opts;

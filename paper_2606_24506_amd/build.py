@@ -16,6 +16,9 @@ LIB = os.path.join(PKG, "libcrosspool.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 # Packed fp32 instructions are disabled for all device code.
 DEVICE_FLAGS = ["--offload-arch=gfx950", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
+# Matrix-core accumulators stay in architectural VGPRs: the decode loops
+# rescale them with vector ops, and AGPR homes would cost a copy each way.
+KERNEL_FLAGS = ["-mllvm", "-amdgpu-mfma-vgpr-form"]
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-function", f"-I{os.path.join(ROOT, 'include')}", f"-I{CSRC}"]
 
 SOURCES = ["api.cpp", "pool.cpp", "kernels.hip"]
@@ -36,7 +39,7 @@ def build(verbose: bool = False) -> str:
     objs = []
     for src in SOURCES:
         obj = os.path.join(objdir, src + ".o")
-        cmd = [HIPCC, *DEVICE_FLAGS, *COMMON, "-c", os.path.join(CSRC, src), "-o", obj]
+        cmd = [HIPCC, *DEVICE_FLAGS, *KERNEL_FLAGS, *COMMON, "-c", os.path.join(CSRC, src), "-o", obj]
         if src.endswith(".cpp"):
             cmd = [HIPCC, *COMMON, "-c", os.path.join(CSRC, src), "-o", obj]
         if verbose:

@@ -20,6 +20,7 @@ _LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libcrosspo
 CP_OK, CP_EINVAL, CP_ENOMEM, CP_ENOSPC, CP_EHIP, CP_ESTATE = 0, -1, -2, -3, -4, -5
 CP_KIND_MLA, CP_KIND_GQA = 0, 1
 CP_PATH_AUTO, CP_PATH_VALU, CP_PATH_MFMA = 0, 1, 2
+CP_SCHED_BALANCED, CP_SCHED_QUEUE, CP_SCHED_GRID = 0, 1, 2
 _NAMES = {0: "CP_OK", -1: "CP_EINVAL", -2: "CP_ENOMEM", -3: "CP_ENOSPC", -4: "CP_EHIP", -5: "CP_ESTATE"}
 
 
@@ -81,7 +82,7 @@ class cp_model_info_t(C.Structure):
 class cp_decode_opts(C.Structure):
     _fields_ = [
         ("num_splits", C.c_int32),
-        ("persistent", C.c_int32),
+        ("schedule", C.c_int32),
         ("path", C.c_int32),
         ("reserved0", C.c_int32),
         ("ev_begin", C.c_void_p),
@@ -233,13 +234,14 @@ def cp_attn_decode(pool: int, req_ids: Sequence[int], q, out, lse, stream=None) 
 
 
 def cp_attn_decode_ex(pool: int, req_ids: Sequence[int], q, out, lse, stream=None, *, num_splits: int = 0,
-                      persistent: int = 1, path: int = CP_PATH_AUTO, ev_begin=None, ev_end=None) -> None:
+                      schedule: int = CP_SCHED_BALANCED, path: int = CP_PATH_AUTO, ev_begin=None,
+                      ev_end=None) -> None:
     def ev(e):
         if e is None:
             return None
         return e.cuda_event if hasattr(e, "cuda_event") else int(e)
 
-    o = cp_decode_opts(num_splits, persistent, path, 0, ev(ev_begin), ev(ev_end))
+    o = cp_decode_opts(num_splits, schedule, path, 0, ev(ev_begin), ev(ev_end))
     _check(LIB.cp_attn_decode_ex(pool, len(req_ids), _i32_array(req_ids), _ptr(q), _ptr(out), _ptr(lse),
                                  _stream(stream), C.byref(o)))
 

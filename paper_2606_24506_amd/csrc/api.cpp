@@ -68,7 +68,7 @@ struct cp_pool {
   bool owns_pool = false;
   uint32_t *dev_pte = nullptr;
   uint32_t *pin_pte = nullptr;  // pinned staging copy of the page table
-  uint32_t *queue = nullptr;    // persistent-grid counters
+  uint32_t *queue = nullptr;    // work-queue counters
   float *ws_o = nullptr;
   float *ws_l = nullptr;
   uint64_t ws_o_cap = 0, ws_l_cap = 0;  // floats
@@ -409,18 +409,19 @@ constexpr int32_t kMatrixFirst = 16;
 // Matrix-core variant for a model, or -1 when none fits its geometry. The
 // matrix path is used where at least 16 query heads share one KV head, so
 // the per-KV-head work is a dense contraction (MLA latent head, MQA, wide
-// GQA groups); it needs page_tokens to be a multiple of 32.
+// GQA groups). The 16- and 32-head variants tile whole 64-token pages; the
+// wider ones need page_tokens to be a multiple of 32.
 int32_t matrix_variant(const Geom &g, int32_t P) {
   if (P % 32) return -1;
   if (g.kind == kMLA && g.latent == 512 && g.rope == 64) {
-    if (g.g == 16) return 16;
-    if (g.g == 32) return 17;
+    if (g.g == 16 && P == 64) return 16;
+    if (g.g == 32 && P == 64) return 17;
     if (g.g == 128) return 18;
     return -1;
   }
   if (g.kind == kGQA && g.head_dim == 128) {
-    if (g.g == 16) return 19;
-    if (g.g == 32) return 20;
+    if (g.g == 16 && P == 64) return 19;
+    if (g.g == 32 && P == 64) return 20;
     if (g.g == 64) return 21;
     if (g.g == 128) return 22;
   }
@@ -463,17 +464,20 @@ cp_status cp_attn_decode_ex(cp_pool *p, int32_t n, const int32_t *req_ids, const
   if (rc) return rc;
   if (!q || !out || !lse) return fail(CP_EINVAL, "null q, out or lse");
   cp_decode_opts o{};
-  o.persistent = 1;
   if (opts) o = *opts;
   if (o.num_splits < 0) return fail(CP_EINVAL, "num_splits must be >= 0");
   if (o.path < CP_PATH_AUTO || o.path > CP_PATH_MFMA) return fail(CP_EINVAL, "unknown path %d", o.path);
+  if (o.schedule < CP_SCHED_BALANCED || o.schedule > CP_SCHED_GRID)
+    return fail(CP_EINVAL, "unknown schedule %d", o.schedule);
+  if (o.schedule == CP_SCHED_BALANCED && o.num_splits != 0)
+    return fail(CP_EINVAL, "num_splits applies to the queue and grid schedules only");
   const int32_t P = p->st.page_tokens();
   for (int32_t i = 0; i < n; ++i) {
     const Request &r = p->st.req(req_ids[i]);
     if (r.ctx_len < 1) return fail(CP_EINVAL, "request %d has an empty context", req_ids[i]);
   }
 
-  // Per-model kernel variant and head blocking.
+  // Per-model kernel variant, head blocking and page cost.
   std::vector<GeomK> gk(p->st.n_models());
   for (int32_t m = 0; m < p->st.n_models(); ++m) {
     const Geom &g = p->st.model(m);
@@ -485,6 +489,10 @@ cp_status cp_attn_decode_ex(cp_pool *p, int32_t n, const int32_t *req_ids, const
     } else {
       choose_valu(g, &gk[m]);
     }
+    // relative work of one page: its bytes, times the head blocks that each
+    // reread it on the MLA vector path
+    const int64_t unit = std::max<int64_t>(1, (g.page_bytes + 8191) / 8192);
+    gk[m].page_cost = (int32_t)(unit * (g.kind == kMLA ? gk[m].nb : 1));
   }
   for (int32_t i = 0; i < n; ++i) {
     const int32_t m = p->st.req(req_ids[i]).model;
@@ -494,9 +502,8 @@ cp_status cp_attn_decode_ex(cp_pool *p, int32_t n, const int32_t *req_ids, const
 
   // Packed offsets in call order.
   std::vector<uint64_t> q_off(n), o_off(n), l_off(n);
+  std::vector<int64_t> pages(n);
   uint64_t qo = 0, oo = 0, lo = 0;
-  std::vector<PlanIn> pin(n);
-  std::vector<int32_t> hblk(n);
   for (int32_t i = 0; i < n; ++i) {
     const Request &r = p->st.req(req_ids[i]);
     const Geom &g = p->st.model(r.model);
@@ -506,54 +513,127 @@ cp_status cp_attn_decode_ex(cp_pool *p, int32_t n, const int32_t *req_ids, const
     qo += (uint64_t)g.hq * g.d_k;
     oo += (uint64_t)g.hq * g.d_v;
     lo += (uint64_t)g.hq;
-    pin[i] = PlanIn{r.model, r.ctx_len};
-    hblk[i] = g.hkv * gk[r.model].nb;
+    pages[i] = (r.ctx_len + P - 1) / P;
   }
   if (qo > 0xFFFFFFFFull || oo > 0xFFFFFFFFull) return fail(CP_EINVAL, "batch too large");
+  auto model_of = [&](int32_t i) { return p->st.req(req_ids[i]).model; };
+  auto wclass = [&](int32_t i) { return decode_waves(gk[model_of(i)].variant); };
 
-  // Work units: about two per CU, or one per CU when every request takes
-  // the 128-head matrix path (its per-unit partials are large); at least
-  // four pages per range so the four waves of a workgroup all get pages.
-  bool all_wide = true, any_matrix = false;
-  for (int32_t i = 0; i < n; ++i) {
-    const int32_t v = gk[p->st.req(req_ids[i]).model].variant;
-    all_wide = all_wide && (v == 18 || v == 22);
-    any_matrix = any_matrix || v >= kMatrixFirst;
-  }
-  std::vector<PlanReq> plan;
-  plan_splits(pin, [&] {
-    std::vector<Geom> v;
-    for (int32_t m = 0; m < p->st.n_models(); ++m) v.push_back(p->st.model(m));
-    return v;
-  }(), P, (int64_t)p->num_cus * (all_wide ? 1 : 2), any_matrix ? 4 : 1, o.num_splits, hblk, &plan);
-  for (auto &pr : plan)
-    if (pr.chunk_pages > 0xFFFF || pr.n_chunks > 0xFFFF) return fail(CP_EINVAL, "context too long to split");
-
-  // Work order: requests whose kernels use the same workgroup size launch
-  // together; inside a launch the costliest units go first (stable in call
-  // order).
-  auto wclass = [&](int32_t i) { return decode_waves(gk[p->st.req(req_ids[i]).model].variant); };
+  // Launch groups: requests whose kernels share a workgroup size, at most
+  // kMaxReqPerLaunch requests and kMaxLaunchModels models each. Within the
+  // queue and grid schedules the costliest units go first.
   std::vector<int32_t> order(n);
   for (int32_t i = 0; i < n; ++i) order[i] = i;
-  std::stable_sort(order.begin(), order.end(), [&](int32_t x, int32_t y) {
-    const int cx = wclass(x), cy = wclass(y);
-    if (cx != cy) return cx < cy;
-    const Geom &gx = p->st.model(p->st.req(req_ids[x]).model);
-    const Geom &gy = p->st.model(p->st.req(req_ids[y]).model);
-    return (double)plan[x].chunk_pages * gx.page_bytes > (double)plan[y].chunk_pages * gy.page_bytes;
-  });
+  std::stable_sort(order.begin(), order.end(), [&](int32_t x, int32_t y) { return wclass(x) < wclass(y); });
+  struct Group {
+    std::vector<int32_t> idx;
+    std::vector<int32_t> models;  // pool model ids, launch-local order
+    uint32_t mask = 0;
+    int grid = 0;
+    uint32_t total_cost = 0;
+    uint32_t n_units = 0;
+  };
+  std::vector<Group> groups;
+  for (int32_t k = 0; k < n;) {
+    Group g;
+    const int cls = wclass(order[k]);
+    while (k < n && (int)g.idx.size() < kMaxReqPerLaunch && wclass(order[k]) == cls) {
+      const int32_t m = model_of(order[k]);
+      if (std::find(g.models.begin(), g.models.end(), m) == g.models.end()) {
+        if ((int)g.models.size() == kMaxLaunchModels) break;
+        g.models.push_back(m);
+      }
+      g.idx.push_back(order[k++]);
+    }
+    for (int32_t m : g.models) g.mask |= 1u << gk[m].variant;
+    groups.push_back(std::move(g));
+  }
 
-  // Workspace for split requests.
+  // Per-request plan: partial slots and the fields the kernels read.
+  std::vector<int32_t> n_slots(n, 1), chunk_pages(n, 0), first_worker(n, 0), hblk(n, 1);
+  std::vector<uint32_t> cost_prefix(n, 0);
+  for (int32_t i = 0; i < n; ++i) {
+    const Geom &g = p->st.model(model_of(i));
+    hblk[i] = g.hkv * gk[model_of(i)].nb;
+  }
+  for (Group &g : groups) {
+    const int wgs = decode_wgs_per_cu(g.mask);
+    const int64_t slots = (int64_t)p->num_cus * wgs;
+    if (o.schedule == CP_SCHED_BALANCED) {
+      uint64_t T = 0, maxc = 1;
+      for (int32_t i : g.idx) {
+        const uint64_t c = (uint64_t)gk[model_of(i)].page_cost;
+        cost_prefix[i] = (uint32_t)T;
+        T += (uint64_t)pages[i] * c;
+        maxc = std::max(maxc, c);
+      }
+      if (T > 0xFFFFFFFFull) return fail(CP_EINVAL, "batch too large for one launch");
+      // every range spans at least one page of any model, so no request has
+      // an empty slot between its first and last worker
+      const uint64_t W = std::max<uint64_t>(1, std::min<uint64_t>((uint64_t)slots, T / maxc));
+      auto owner = [&](uint64_t x) { return (uint32_t)(((x + 1) * W - 1) / T); };
+      for (int32_t i : g.idx) {
+        const uint64_t c = (uint64_t)gk[model_of(i)].page_cost, C = cost_prefix[i];
+        const uint32_t w0 = owner(C), w1 = owner(C + (uint64_t)(pages[i] - 1) * c);
+        first_worker[i] = (int32_t)w0;
+        n_slots[i] = (int32_t)(w1 - w0 + 1);
+      }
+      g.grid = (int)W;
+      g.total_cost = (uint32_t)T;
+    } else {
+      // queue / grid: page-aligned KV ranges of similar cost, about two per
+      // workgroup slot (one when every request is a 128-head matrix model,
+      // whose partials are large); at least four pages per range on the
+      // matrix path so all waves of a workgroup get pages
+      bool all_wide = true, any_matrix = false;
+      std::vector<PlanIn> pin;
+      std::vector<int32_t> hb;
+      for (int32_t i : g.idx) {
+        const int32_t v = gk[model_of(i)].variant;
+        all_wide = all_wide && (v == 18 || v == 22);
+        any_matrix = any_matrix || v >= kMatrixFirst;
+        pin.push_back(PlanIn{model_of(i), p->st.req(req_ids[i]).ctx_len});
+        hb.push_back(hblk[i]);
+      }
+      std::vector<Geom> geoms;
+      for (int32_t m = 0; m < p->st.n_models(); ++m) geoms.push_back(p->st.model(m));
+      std::vector<PlanReq> plan;
+      plan_splits(pin, geoms, P, slots * (all_wide ? 1 : 2), any_matrix ? 4 : 1, o.num_splits, hb, &plan);
+      // costliest units first
+      std::vector<int32_t> pos(g.idx.size());
+      for (size_t k = 0; k < pos.size(); ++k) pos[k] = (int32_t)k;
+      std::stable_sort(pos.begin(), pos.end(), [&](int32_t x, int32_t y) {
+        const Geom &gx = p->st.model(model_of(g.idx[x])), &gy = p->st.model(model_of(g.idx[y]));
+        return (double)plan[x].chunk_pages * gx.page_bytes > (double)plan[y].chunk_pages * gy.page_bytes;
+      });
+      std::vector<int32_t> idx2;
+      uint32_t units = 0;
+      for (int32_t k : pos) {
+        const int32_t i = g.idx[k];
+        if (plan[k].chunk_pages > 0xFFFF || plan[k].n_chunks > 0xFFFF) return fail(CP_EINVAL, "context too long to split");
+        chunk_pages[i] = plan[k].chunk_pages;
+        n_slots[i] = plan[k].n_chunks;
+        cost_prefix[i] = units;  // first unit
+        units += (uint32_t)plan[k].n_chunks * (uint32_t)hblk[i];
+        idx2.push_back(i);
+      }
+      g.idx = idx2;
+      g.n_units = units;
+      g.grid = o.schedule == CP_SCHED_QUEUE ? (int)std::min<int64_t>(units, slots) : (int)units;
+    }
+  }
+
+  // Workspace for requests split over several slots.
   uint64_t ws_rows = 0, ws_floats = 0;
   std::vector<uint32_t> ws_base(n, kNoWs), ws_orow(n, 0);
   for (int32_t i = 0; i < n; ++i) {
-    if (plan[i].n_chunks <= 1) continue;
-    const Geom &g = p->st.model(p->st.req(req_ids[i]).model);
+    if (n_slots[i] <= 1) continue;
+    const Geom &g = p->st.model(model_of(i));
     ws_base[i] = (uint32_t)ws_rows;
-    ws_rows += (uint64_t)plan[i].n_chunks * g.hq;
+    ws_rows += (uint64_t)n_slots[i] * g.hq;
     ws_floats = (ws_floats + 511) / 512 * 512;
     ws_orow[i] = (uint32_t)(ws_floats / (uint64_t)g.d_v);
-    ws_floats += (uint64_t)plan[i].n_chunks * g.hq * g.d_v;
+    ws_floats += (uint64_t)n_slots[i] * g.hq * g.d_v;
   }
   if (ws_rows >= kNoWs || ws_floats / 64 >= kNoWs) return fail(CP_EINVAL, "split workspace too large");
 
@@ -563,14 +643,11 @@ cp_status cp_attn_decode_ex(cp_pool *p, int32_t n, const int32_t *req_ids, const
     rc = ensure_ws(p, ws_floats, ws_rows);
     if (rc) return rc;
   }
-
   if (o.ev_begin) {
     hipError_t e = hipEventRecord((hipEvent_t)o.ev_begin, s);
     if (e != hipSuccess) return hip_fail(e, "event record");
   }
-  // Decode launches in groups.
-  int32_t idx = 0;
-  while (idx < n) {
+  for (const Group &g : groups) {
     DecodeArgs a{};
     a.pool = p->dev_pool;
     a.pte = p->dev_pte;
@@ -580,19 +657,12 @@ cp_status cp_attn_decode_ex(cp_pool *p, int32_t n, const int32_t *req_ids, const
     a.ws_o = p->ws_o;
     a.ws_l = p->ws_l;
     a.queue = p->queue;
-    int32_t nm = 0, model_map[16];
-    for (int k = 0; k < 16; ++k) model_map[k] = -1;
-    uint32_t units = 0;
-    const int cls = wclass(order[idx]);
-    while (idx < n && a.n_req < kMaxReqPerLaunch && wclass(order[idx]) == cls) {
-      const int32_t i = order[idx];
+    a.schedule = o.schedule;
+    a.total_cost = g.total_cost;
+    a.n_units = (int32_t)g.n_units;
+    for (size_t k = 0; k < g.models.size(); ++k) a.geom[k] = gk[g.models[k]];
+    for (int32_t i : g.idx) {
       const Request &r = p->st.req(req_ids[i]);
-      int32_t mi = model_map[r.model];
-      if (mi < 0) {
-        if (nm == kMaxLaunchModels) break;
-        mi = model_map[r.model] = nm;
-        a.geom[nm++] = gk[r.model];
-      }
       DecReq &d = a.req[a.n_req++];
       d.pte_base = r.pte_base;
       d.ctx_len = (uint32_t)r.ctx_len;
@@ -601,22 +671,14 @@ cp_status cp_attn_decode_ex(cp_pool *p, int32_t n, const int32_t *req_ids, const
       d.lse_off = (uint32_t)l_off[i];
       d.ws_base = ws_base[i];
       d.ws_orow = ws_orow[i];
-      d.unit_begin = units;
-      d.chunk_pages = (uint16_t)plan[i].chunk_pages;
-      d.n_chunks = (uint16_t)plan[i].n_chunks;
-      d.model = (uint8_t)mi;
-      d.n_hblk = (uint16_t)plan[i].n_hblk;
-      units += (uint32_t)plan[i].n_chunks * (uint32_t)plan[i].n_hblk;
-      ++idx;
+      d.unit_begin = cost_prefix[i];
+      d.chunk_pages = (uint16_t)(o.schedule == CP_SCHED_BALANCED ? first_worker[i] : chunk_pages[i]);
+      d.n_chunks = (uint16_t)n_slots[i];
+      d.model = (uint8_t)(std::find(g.models.begin(), g.models.end(), r.model) - g.models.begin());
+      d.n_hblk = (uint16_t)hblk[i];
     }
-    a.n_units = (int32_t)units;
-    a.persistent = o.persistent ? 1 : 0;
-    uint32_t mask = 0;
-    for (int32_t k = 0; k < nm; ++k) mask |= 1u << a.geom[k].variant;
-    int grid = (int)units;
-    if (a.persistent)
-      grid = (int)std::min<uint32_t>(units, (uint32_t)p->num_cus * (uint32_t)decode_wgs_per_cu(mask));
-    hipError_t e = launch_decode(a, grid, mask, s);
+    if (g.grid > 0xFFFF && o.schedule == CP_SCHED_BALANCED) return fail(CP_EINVAL, "too many workers");
+    hipError_t e = launch_decode(a, g.grid, g.mask, s);
     if (e != hipSuccess) return hip_fail(e, "decode launch");
   }
   if (o.ev_end) {
@@ -635,7 +697,7 @@ cp_status cp_attn_decode_ex(cp_pool *p, int32_t n, const int32_t *req_ids, const
     hipError_t e = launch_merge(ma, s);
     if (e != hipSuccess) return hip_fail(e, "merge launch");
     ma.n_req = 0;
-    ma.total_heads = 0;
+    ma.n_blocks = 0;
     return CP_OK;
   };
   for (int32_t i = 0; i < n; ++i) {
@@ -644,17 +706,18 @@ cp_status cp_attn_decode_ex(cp_pool *p, int32_t n, const int32_t *req_ids, const
       rc = flush();
       if (rc) return rc;
     }
-    const Geom &g = p->st.model(p->st.req(req_ids[i]).model);
+    const Geom &g = p->st.model(model_of(i));
     MergeReq &m = ma.req[ma.n_req++];
-    m.head_begin = (uint32_t)ma.total_heads;
+    m.block_begin = (uint32_t)ma.n_blocks;  // first merge workgroup of this request
     m.hq = (uint32_t)g.hq;
     m.d_v = (uint32_t)g.d_v;
-    m.n_chunks = (uint32_t)plan[i].n_chunks;
+    m.n_chunks = (uint32_t)n_slots[i];
     m.ws_base = ws_base[i];
     m.ws_orow = ws_orow[i];
     m.o_off = (uint32_t)o_off[i];
     m.lse_off = (uint32_t)l_off[i];
-    ma.total_heads += g.hq;
+    // one workgroup per (head, block of 128 V columns)
+    ma.n_blocks += g.hq * std::max(1, g.d_v / 128);
   }
   return flush();
 }

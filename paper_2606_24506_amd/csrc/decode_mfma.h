@@ -30,7 +30,7 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
 constexpr int kLdsBuf = 77824;  // bytes per KV buffer (two buffers)
-constexpr int kRedFloats = 2 * 4 * 128 + 2 * 128;
+constexpr int kRedFloats = 1536;  // reduction / exchange floats
 constexpr float kLazy = 8.0f;  // log2 headroom before the softmax reference moves
 
 // Direct HBM -> LDS load of 16 bytes per lane: lane i writes
@@ -42,6 +42,20 @@ constexpr float kLazy = 8.0f;  // log2 headroom before the softmax reference mov
 #pragma clang diagnostic ignored "-Winline-asm"
 CP_DEV void dma16(const void *g, uint32_t lds_base) {
   asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(lds_base) : "memory", "m0");
+}
+// Same with a wave-uniform base address in SGPRs and a 32-bit per-lane
+// byte offset.
+CP_DEV void dma16_sbase(uint64_t sbase, uint32_t voff, uint32_t lds_base) {
+  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(voff), "s"(sbase), "s"(lds_base)
+               : "memory", "m0");
+}
+
+// A pointer known to be the same in every lane, moved to scalar registers.
+CP_DEV uint64_t uniform_ptr(const void *p) {
+  const uint64_t v = (uint64_t)(uintptr_t)p;
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
+  return ((uint64_t)hi << 32) | lo;
 }
 #pragma clang diagnostic pop
 
@@ -69,6 +83,11 @@ struct MfmaCfg {
   static constexpr int NBLK = DV / 16;
   static constexpr int HEADS = 16 * HBW * WPT;  // query heads per KV head
   static constexpr int BUF = GROUPS * TILE;     // bytes of one of the two KV buffers
+  // LDS fragment batches of the software pipelines (smaller when 8 waves
+  // share a SIMD pair and registers are scarce)
+  static constexpr int KB = KSTEPS % 6 == 0 && NW < 8 ? 6 : (KSTEPS % 3 == 0 ? 3 : 2);
+  static constexpr int VB = NW < 8 ? 8 : 4;
+  static_assert(KSTEPS % KB == 0 && NBLK % VB == 0, "batches must tile the steps");
   static_assert(BUF <= kLdsBuf, "tile does not fit");
   static_assert(GROUPS == 1 || WPT == 1, "streams of several waves need their own barriers");
   static_assert(DMA_WAVE <= 24, "too many loads in flight per wave");
@@ -78,8 +97,9 @@ struct MfmaCfg {
 // Waves form GROUPS tile streams of WPT waves; a stream takes every
 // GROUPS-th page of the range, and its WPT waves split the head blocks.
 template <int HBW, int WPT, int NW, int DK, int DV, int T, bool MLA>
-__device__ __forceinline__ void mfma_unit(const DecodeArgs &a, const GeomK &gm, const DecReq &rq, uint32_t chunk,
-                                          uint32_t kvh, char *buf0, char *buf1, float *red) {
+__device__ __forceinline__ void mfma_unit(const DecodeArgs &a, const GeomK &gm, const DecReq &rq, const Seg &sg,
+                                          char *buf0, char *buf1, float *red) {
+  const uint32_t kvh = sg.hblk, chunk = sg.slot;
   using C = MfmaCfg<HBW, WPT, NW, DK, DV, T, MLA>;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int grp = wave / WPT, wig = wave % WPT;
@@ -96,49 +116,62 @@ __device__ __forceinline__ void mfma_unit(const DecodeArgs &a, const GeomK &gm, 
       qf[hb][c] = *reinterpret_cast<const bf16x8 *>(a.q + rq.q_off + (uint32_t)(h_wave + 16 * hb + col) * DK +
                                                    32 * c + 8 * quad);
 
-  const uint32_t tok_begin = chunk * rq.chunk_pages * (uint32_t)P;
-  const uint32_t tok_end = min(rq.ctx_len, tok_begin + (uint32_t)rq.chunk_pages * P);
-  const uint32_t pg_begin = chunk * rq.chunk_pages;
+  const uint32_t tok_end = min(rq.ctx_len, sg.pg_end * (uint32_t)P);
+  const uint32_t pg_begin = sg.pg_begin;
   const uint32_t pg_end = (tok_end + P - 1) / P;
   const int tpp = P / T;  // tiles per page
-  // this stream's pages: pg_begin + grp + GROUPS*i
-  const int npg = (int)pg_end - (int)pg_begin > grp ? ((int)(pg_end - pg_begin) - grp + C::GROUPS - 1) / C::GROUPS : 0;
-  int ntiles = 0;
-  if (npg > 0) {
-    const uint32_t lp = pg_begin + grp + C::GROUPS * (npg - 1);
-    const int last_tok = (int)min(tok_end, (lp + 1) * (uint32_t)P) - (int)(lp * P);
-    ntiles = (npg - 1) * tpp + (last_tok + T - 1) / T;
-  }
+  // The segment's tiles in page-major order; stream grp takes tiles grp,
+  // grp + GROUPS, ... so streams differ by at most one tile of work.
+  const int npg = (int)pg_end - (int)pg_begin;
+  const int last_tok = npg > 0 ? (int)tok_end - (int)((pg_end - 1) * (uint32_t)P) : 0;
+  const int seg_tiles = npg > 0 ? (npg - 1) * tpp + (last_tok + T - 1) / T : 0;
+  const int ntiles = seg_tiles > grp ? (seg_tiles - grp + C::GROUPS - 1) / C::GROUPS : 0;
   const uint64_t kv_head_bytes = MLA ? 0 : (uint64_t)2 * P * DK * 2;
   char *const tb0 = buf0 + grp * C::TILE;
   char *const tb1 = buf1 + grp * C::TILE;
 
+  // Page-table entries of the segment's pages, 64 at a time: lane i holds
+  // the entry of page (64 * batch + i). Loading them ahead of the tile loop
+  // keeps vector loads of the page table (and the full vmcnt wait the
+  // compiler puts after them) out of the per-tile path.
+  uint32_t pte_lane = 0;
+  int pte_batch = -1;
+  auto load_ptes = [&](int batch) {
+    const int sp = batch * 64 + lane;  // page index within the segment
+    pte_lane = sp < npg ? a.pte[rq.pte_base + pg_begin + (uint32_t)sp] : 0u;
+    pte_batch = batch;
+  };
+
   // Issue the direct loads of tile k into tile buffer `dst`.
   auto issue = [&](int k, char *dst) {
-    const uint32_t page = pg_begin + grp + C::GROUPS * (uint32_t)(k / tpp);
-    const uint32_t t0 = (uint32_t)(k % tpp) * T;
-    const uint32_t pte = __builtin_amdgcn_readfirstlane(a.pte[rq.pte_base + page]);
-    const uint8_t *base = a.pool + ((uint64_t)pte << 8) + kvh * kv_head_bytes;
-    const uint8_t *srck = base + (uint64_t)t0 * C::KROW;
-    const uint8_t *srcv = base + (uint64_t)P * DK * 2 + (uint64_t)t0 * C::VROW;
+    const int t = grp + C::GROUPS * k;  // tile within the segment
+    const int sp = t / tpp;
+    if ((sp >> 6) != pte_batch) load_ptes(sp >> 6);
+    const uint32_t t0 = (uint32_t)(t % tpp) * T;
+    const uint32_t pte = __builtin_amdgcn_readlane(pte_lane, sp & 63);
+    // uniform base of the KV head's block in this page; K rows of the tile
+    // start t0 rows in, V rows P rows after the K rows (GQA layout)
+    const uint8_t *base = a.pool + ((uint64_t)pte << 8) + kvh * kv_head_bytes + (uint64_t)t0 * C::KROW;
     const uint32_t ldsb = lds_addr(dst);
+    const uint64_t sbase = uniform_ptr(base);
 #pragma unroll
     for (int i = 0; i < C::DMA_WAVE; ++i) {
       const int inst = wig * C::DMA_WAVE + i;
       const int o = inst * 1024 + lane * 16;  // byte offset inside the LDS tile
-      const uint8_t *g = nullptr;
-      bool use = false;
-      if (o < C::TILE_K) {
-        const int row = o / C::KPITCH, w = o - row * C::KPITCH;
-        use = w < C::KROW;
-        g = srck + row * C::KROW + w;
-      } else if (o < C::TILE_USED) {
-        const int o2 = o - C::TILE_K;
+      // Lanes that land on a row's 16-byte pad, or past the tile, fetch the
+      // first 16 bytes of a row they already cover (same cache lines), so
+      // every load is issued by all lanes without branches.
+      uint32_t off;
+      if (C::TILE_V == 0 || o < C::TILE_K) {
+        const int oc = o < C::TILE_K ? o : 0;
+        const int row = oc / C::KPITCH, w = oc - row * C::KPITCH;
+        off = (uint32_t)(row * C::KROW + (w < C::KROW ? w : 0));
+      } else {
+        const int o2 = o < C::TILE_USED ? o - C::TILE_K : 0;
         const int row = o2 / C::VPITCH, w = o2 - row * C::VPITCH;
-        use = w < C::VROW;
-        g = srcv + row * C::VROW + w;
+        off = (uint32_t)(P * DK * 2 + row * C::VROW + (w < C::VROW ? w : 0));
       }
-      if (use) dma16(g, __builtin_amdgcn_readfirstlane(ldsb + inst * 1024));
+      dma16_sbase(sbase, off, __builtin_amdgcn_readfirstlane(ldsb + inst * 1024));
     }
   };
 
@@ -154,8 +187,8 @@ __device__ __forceinline__ void mfma_unit(const DecodeArgs &a, const GeomK &gm, 
   const float sl2 = gm.scale_log2;
 
   auto compute = [&](int k, char *tb) {
-    const uint32_t page = pg_begin + grp + C::GROUPS * (uint32_t)(k / tpp);
-    const int t0 = (int)(page * P) + (k % tpp) * T;  // first token of the tile
+    const int t = grp + C::GROUPS * k;  // tile within the segment
+    const int t0 = (int)((pg_begin + (uint32_t)(t / tpp)) * P) + (t % tpp) * T;  // first token of the tile
     const int valid = min(T, (int)tok_end - t0);
     const char *kt = tb;
     char *vt = MLA ? tb : tb + C::TILE_K;
@@ -174,19 +207,43 @@ __device__ __forceinline__ void mfma_unit(const DecodeArgs &a, const GeomK &gm, 
     const int va = col & 3;
 #pragma unroll 1
     for (int sub = 0; sub < C::NSUB; ++sub) {
-      f32x4 s[HBW];
+      // NACC independent accumulators break the dependent MFMA chain
+      constexpr int NACC = C::KSTEPS % 3 == 0 ? 3 : 2;
+      f32x4 s[HBW], sacc[NACC][HBW];
 #pragma unroll
-      for (int hb = 0; hb < HBW; ++hb) s[hb] = f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int hb = 0; hb < HBW; ++hb)
+#pragma unroll
+        for (int u = 0; u < NACC; ++u) sacc[u][hb] = f32x4{0.f, 0.f, 0.f, 0.f};
       {
+        // K fragments in batches of KB: batch b+1 is read while batch b
+        // feeds the matrix cores.
         const char *kr = kt + (sub * 16 + col) * C::KPITCH + quad * 16;
+        constexpr int KB = C::KB, NKB = C::KSTEPS / KB;
+        bf16x8 kf[2][KB];
 #pragma unroll
-        for (int c = 0; c < C::KSTEPS; ++c) {
-          const bf16x8 kf = *reinterpret_cast<const bf16x8 *>(kr + 64 * c);
+        for (int j = 0; j < KB; ++j) kf[0][j] = *reinterpret_cast<const bf16x8 *>(kr + 64 * j);
 #pragma unroll
-          for (int hb = 0; hb < HBW; ++hb) s[hb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[hb][c], s[hb], 0, 0, 0);
-          // keep at most a few K fragments in flight (bounds VGPR use)
-          if ((c & 3) == 3) __builtin_amdgcn_sched_barrier(0);
+        for (int b = 0; b < NKB; ++b) {
+          if (b + 1 < NKB) {
+#pragma unroll
+            for (int j = 0; j < KB; ++j)
+              kf[(b + 1) & 1][j] = *reinterpret_cast<const bf16x8 *>(kr + 64 * ((b + 1) * KB + j));
+          }
+#pragma unroll
+          for (int j = 0; j < KB; ++j) {
+            const int u = (b * KB + j) % NACC;
+#pragma unroll
+            for (int hb = 0; hb < HBW; ++hb)
+              sacc[u][hb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[b & 1][j], qf[hb][b * KB + j], sacc[u][hb], 0, 0, 0);
+          }
+          __builtin_amdgcn_sched_barrier(0);
         }
+      }
+#pragma unroll
+      for (int hb = 0; hb < HBW; ++hb) {
+        s[hb] = sacc[0][hb];
+#pragma unroll
+        for (int u = 1; u < NACC; ++u) s[hb] += sacc[u][hb];
       }
       // Online softmax; lane owns head column `col`, tokens sub*16 + 4*quad + r.
       // The reference maximum m only moves when the slice maximum exceeds it
@@ -238,20 +295,37 @@ __device__ __forceinline__ void mfma_unit(const DecodeArgs &a, const GeomK &gm, 
       // O^T += V^T P^T; the transpose read gives lane (4a+b) of each 16-lane
       // quarter column (4a+b) of four V rows supplied by lanes a, 4+a, 8+a, 12+a.
       const char *vr = vt + (sub * 16 + vrow_l) * C::VPITCH + 8 * va;
+      {
+        // V^T fragments in batches of VB, software-pipelined like K.
+        constexpr int VB = C::VB, NVB = C::NBLK / VB;
+        s16x4 vf[2][VB];
 #pragma unroll
-      for (int nb = 0; nb < C::NBLK; ++nb) {
-        const s16x4 vf = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-            (__attribute__((address_space(3))) s16x4 *)(vr + 32 * nb));
+        for (int j = 0; j < VB; ++j)
+          vf[0][j] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4 *)(vr + 32 * j));
 #pragma unroll
-        for (int hb = 0; hb < HBW; ++hb)
-          o[hb][nb] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vf, pf[hb], o[hb][nb], 0, 0, 0);
-        if ((nb & 3) == 3) __builtin_amdgcn_sched_barrier(0);
+        for (int b = 0; b < NVB; ++b) {
+          if (b + 1 < NVB) {
+#pragma unroll
+            for (int j = 0; j < VB; ++j)
+              vf[(b + 1) & 1][j] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                  (__attribute__((address_space(3))) s16x4 *)(vr + 32 * ((b + 1) * VB + j)));
+          }
+#pragma unroll
+          for (int j = 0; j < VB; ++j)
+#pragma unroll
+            for (int hb = 0; hb < HBW; ++hb)
+              o[hb][b * VB + j] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vf[b & 1][j], pf[hb], o[hb][b * VB + j], 0, 0, 0);
+          __builtin_amdgcn_sched_barrier(0);
+        }
       }
     }
   };
 
   // Double-buffered tile loop: tile k+1 streams in while tile k is used.
-  if (ntiles > 0) issue(0, tb0);
+  if (ntiles > 0) {
+    load_ptes(0);
+    issue(0, tb0);
+  }
 #pragma unroll 1
   for (int k = 0; k < ntiles; ++k) {
     char *cur = (k & 1) ? tb1 : tb0;

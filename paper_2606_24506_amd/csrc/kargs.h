@@ -10,6 +10,13 @@ namespace cp {
 constexpr int kMaxLaunchModels = 4;   // distinct models in one decode launch
 constexpr int kMaxReqPerLaunch = 64;  // requests in one launch
 constexpr uint32_t kNoWs = 0xFFFFFFFFu;
+enum : int32_t { kSchedBalanced = 0, kSchedQueue = 1, kSchedGrid = 2 };
+
+// One piece of decode work: pages [pg_begin, pg_end) of a request, for one
+// head block, writing partial slot `slot` when the request is split.
+struct Seg {
+  uint32_t pg_begin, pg_end, slot, hblk;
+};
 
 // Per-model geometry as the kernels see it.
 struct GeomK {
@@ -20,6 +27,7 @@ struct GeomK {
   int32_t variant;     // kernel code path chosen by the host
   float scale_log2;    // softmax scale * log2(e)
   int32_t nb;          // head blocks per KV head (vector path)
+  int32_t page_cost;   // relative work of one page (balanced schedule)
 };
 
 // One request of a decode launch.
@@ -31,9 +39,9 @@ struct DecReq {
   uint32_t lse_off;   // float offset of its log-sum-exp values
   uint32_t ws_base;   // first partial lse row (kNoWs when the request is not split)
   uint32_t ws_orow;   // partial outputs start at float offset ws_orow * d_v
-  uint32_t unit_begin;
-  uint16_t chunk_pages;  // pages per KV range
-  uint16_t n_chunks;     // KV ranges
+  uint32_t unit_begin;   // queue/grid: first unit; balanced: cost prefix of the request
+  uint16_t chunk_pages;  // queue/grid: pages per KV range; balanced: first worker of the request
+  uint16_t n_chunks;     // KV ranges = partial slots
   uint8_t model;         // index into DecodeArgs::geom
   uint8_t pad;
   uint16_t n_hblk;       // head blocks per KV range
@@ -47,14 +55,16 @@ struct DecodeArgs {
   float *lse;
   float *ws_o;        // partial outputs, [row][d_v] fp32, normalised
   float *ws_l;        // partial log-sum-exp, [row], natural log
-  uint32_t *queue;    // persistent mode: {next unit, finished workgroups}
-  int32_t n_req, n_units, persistent, pad;
+  uint32_t *queue;    // queue schedule: {next unit, finished workgroups}
+  int32_t n_req, n_units;
+  int32_t schedule;     // kSchedBalanced, kSchedQueue or kSchedGrid
+  uint32_t total_cost;  // balanced: summed page costs of the launch
   GeomK geom[kMaxLaunchModels];
   DecReq req[kMaxReqPerLaunch];
 };
 
 struct MergeReq {
-  uint32_t head_begin;  // first merge row of this request in the grid
+  uint32_t block_begin;  // first merge workgroup of this request
   uint32_t hq, d_v, n_chunks;
   uint32_t ws_base, ws_orow, o_off, lse_off;
 };
@@ -64,7 +74,7 @@ struct MergeArgs {
   const float *ws_l;
   uint16_t *out;
   float *lse;
-  int32_t n_req, total_heads, pad0, pad1;
+  int32_t n_req, n_blocks, pad0, pad1;  // n_blocks: merge workgroups
   MergeReq req[kMaxReqPerLaunch];
 };
 

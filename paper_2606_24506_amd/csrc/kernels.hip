@@ -9,6 +9,7 @@
 // A page starts at pool + (pte << 8).
 #include <hip/hip_runtime.h>
 
+#include "decode_coop.h"
 #include "decode_mfma.h"
 #include "device_common.h"
 #include "kargs.h"
@@ -98,8 +99,9 @@ constexpr int kLdsFloats = 16 * 1024 + 4 * 2 * 16 + 64;
 // its own online-softmax state; the four states are combined at the end in
 // a fixed order. Scores live in the log2 domain: s2 = scale*log2(e)*<q, k>.
 template <int HB, int DPL>
-__device__ __forceinline__ void valu_unit(const DecodeArgs &a, const GeomK &gm, const DecReq &rq, uint32_t chunk, uint32_t hblk,
-                          float *lds) {
+__device__ __forceinline__ void valu_unit(const DecodeArgs &a, const GeomK &gm, const DecReq &rq, const Seg &sg,
+                                          float *lds) {
+  const uint32_t chunk = sg.slot, hblk = sg.hblk;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int P = gm.page_tokens;
   const int kvh = (int)hblk / gm.nb, hbi = (int)hblk % gm.nb;
@@ -114,9 +116,8 @@ __device__ __forceinline__ void valu_unit(const DecodeArgs &a, const GeomK &gm, 
   }
   __syncthreads();
 
-  const uint32_t tok_begin = chunk * rq.chunk_pages * (uint32_t)P;
-  const uint32_t tok_end = min(rq.ctx_len, tok_begin + (uint32_t)rq.chunk_pages * P);
-  const uint32_t pg_begin = chunk * rq.chunk_pages;
+  const uint32_t tok_end = min(rq.ctx_len, sg.pg_end * (uint32_t)P);
+  const uint32_t pg_begin = sg.pg_begin;
   const uint32_t pg_end = (tok_end + P - 1) / P;
   const uint64_t head_blk = gm.kind == 0 ? 0 : (uint64_t)2 * P * dk * 2;
   const uint32_t stride = (uint32_t)dk * 2;
@@ -258,18 +259,16 @@ enum : int32_t {
 };
 
 template <int V> struct Mcfg;
-template <> struct Mcfg<kM_MLA_G16> { using C = MfmaCfg<1, 1, 4, 576, 512, 16, true>; };
-template <> struct Mcfg<kM_MLA_G32> { using C = MfmaCfg<1, 2, 2, 576, 512, 16, true>; };
+template <> struct Mcfg<kM_MLA_G16> { using C = CoopCfg<1, 576, 512, true, 2, 3>; };
+template <> struct Mcfg<kM_MLA_G32> { using C = CoopCfg<2, 576, 512, true, 2, 3>; };
 template <> struct Mcfg<kM_MLA_G128> { using C = MfmaCfg<1, 8, 8, 576, 512, 32, true>; };
-template <> struct Mcfg<kM_D128_G16> { using C = MfmaCfg<1, 1, 4, 128, 128, 32, false>; };
-template <> struct Mcfg<kM_D128_G32> { using C = MfmaCfg<2, 1, 4, 128, 128, 32, false>; };
+template <> struct Mcfg<kM_D128_G16> { using C = CoopCfg<1, 128, 128, false, 4, 3>; };
+template <> struct Mcfg<kM_D128_G32> { using C = CoopCfg<2, 128, 128, false, 4, 3>; };
 template <> struct Mcfg<kM_D128_G64> { using C = MfmaCfg<4, 1, 4, 128, 128, 32, false>; };
 template <> struct Mcfg<kM_D128_G128> { using C = MfmaCfg<2, 4, 4, 128, 128, 32, false>; };
 
 // Waves per workgroup of each variant (vector variants use four).
-constexpr int variant_waves(int v) {
-  return v == kM_MLA_G32 ? 2 : v == kM_MLA_G128 ? 8 : 4;
-}
+constexpr int variant_waves(int v) { return v == kM_MLA_G128 ? 8 : 4; }
 
 template <int V>
 constexpr int mcfg_buf() { return Mcfg<V>::C::BUF; }
@@ -288,18 +287,14 @@ constexpr int kernel_buf_bytes(uint32_t mask) {
 }
 
 template <uint32_t MASK>
-__device__ __forceinline__ void run_unit(const DecodeArgs &a, uint32_t u, char *buf0, char *buf1, float *red) {
-  int r = 0;
-  while (r + 1 < a.n_req && a.req[r + 1].unit_begin <= u) ++r;
-  const DecReq &rq = a.req[r];
+__device__ __forceinline__ void run_seg(const DecodeArgs &a, const DecReq &rq, const Seg &sg, char *buf0, char *buf1,
+                                        float *red) {
   const GeomK &gm = a.geom[rq.model];
-  const uint32_t local = u - rq.unit_begin;
-  const uint32_t chunk = local / rq.n_hblk, hblk = local % rq.n_hblk;
   float *lds = reinterpret_cast<float *>(buf0);
 #define CP_VCASE(V, HB, DPL)                                        \
   if constexpr (has(MASK, V)) {                                     \
     if (gm.variant == V) {                                          \
-      valu_unit<HB, DPL>(a, gm, rq, chunk, hblk, lds);              \
+      valu_unit<HB, DPL>(a, gm, rq, sg, lds);                       \
       return;                                                       \
     }                                                               \
   }
@@ -309,26 +304,87 @@ __device__ __forceinline__ void run_unit(const DecodeArgs &a, uint32_t u, char *
 #define CP_MCASE(V, HBW, WPT, NW, DK, DV, T, MLA)                                    \
   if constexpr (has(MASK, V)) {                                                      \
     if (gm.variant == V) {                                                           \
-      mfma_unit<HBW, WPT, NW, DK, DV, T, MLA>(a, gm, rq, chunk, hblk, buf0, buf1, red); \
+      mfma_unit<HBW, WPT, NW, DK, DV, T, MLA>(a, gm, rq, sg, buf0, buf1, red);       \
       return;                                                                        \
     }                                                                                \
   }
-  CP_MCASE(kM_MLA_G16, 1, 1, 4, 576, 512, 16, true)
-  CP_MCASE(kM_MLA_G32, 1, 2, 2, 576, 512, 16, true)
+#define CP_CCASE(V, HBW, DK, DV, MLA, NS, NBUF)                                      \
+  if constexpr (has(MASK, V)) {                                                      \
+    if (gm.variant == V) {                                                           \
+      coop_unit<HBW, DK, DV, MLA, NS, NBUF>(a, gm, rq, sg, buf0, buf1, red);         \
+      return;                                                                        \
+    }                                                                                \
+  }
+  CP_CCASE(kM_MLA_G16, 1, 576, 512, true, 2, 3)
+  CP_CCASE(kM_MLA_G32, 2, 576, 512, true, 2, 3)
+  CP_CCASE(kM_D128_G16, 1, 128, 128, false, 4, 3)
+  CP_CCASE(kM_D128_G32, 2, 128, 128, false, 4, 3)
+#undef CP_CCASE
   CP_MCASE(kM_MLA_G128, 1, 8, 8, 576, 512, 32, true)
-  CP_MCASE(kM_D128_G16, 1, 1, 4, 128, 128, 32, false)
-  CP_MCASE(kM_D128_G32, 2, 1, 4, 128, 128, 32, false)
   CP_MCASE(kM_D128_G64, 4, 1, 4, 128, 128, 32, false)
   CP_MCASE(kM_D128_G128, 2, 4, 4, 128, 128, 32, false)
 #undef CP_MCASE
 }
 
-// Work loop shared by the decode kernels. Persistent mode: workgroups pull
+// Queue and grid schedules: unit u is (request, KV range, head block).
+template <uint32_t MASK>
+__device__ __forceinline__ void run_unit(const DecodeArgs &a, uint32_t u, char *buf0, char *buf1, float *red) {
+  int r = 0;
+  while (r + 1 < a.n_req && a.req[r + 1].unit_begin <= u) ++r;
+  const DecReq &rq = a.req[r];
+  const uint32_t local = u - rq.unit_begin;
+  const uint32_t chunk = local / rq.n_hblk;
+  const uint32_t pages = (rq.ctx_len + a.geom[rq.model].page_tokens - 1) / a.geom[rq.model].page_tokens;
+  Seg sg;
+  sg.pg_begin = chunk * rq.chunk_pages;
+  sg.pg_end = min(pages, sg.pg_begin + rq.chunk_pages);
+  sg.slot = chunk;
+  sg.hblk = local % rq.n_hblk;
+  run_seg<MASK>(a, rq, sg, buf0, buf1, red);
+}
+
+// Balanced schedule. The launch's requests, in order, form one sequence of
+// pages; page j of request r covers costs [C_r + j c_r, C_r + (j+1) c_r)
+// with C_r the cost prefix and c_r its model's page cost. Workgroup w owns
+// the pages whose first cost lies in [w T / W, (w+1) T / W) (T the total
+// cost, W the grid), so every workgroup gets the same work to within one
+// page. Its pages of request r land in partial slot w - w_first(r).
+template <uint32_t MASK>
+__device__ __forceinline__ void run_balanced(const DecodeArgs &a, char *buf0, char *buf1, float *red) {
+  const uint64_t W = gridDim.x, w = blockIdx.x, T = a.total_cost;
+  const uint64_t L0 = w * T / W, L1 = (w + 1) * T / W;
+  for (int r = 0; r < a.n_req; ++r) {
+    const DecReq &rq = a.req[r];
+    const GeomK &gm = a.geom[rq.model];
+    const uint64_t C = rq.unit_begin, c = (uint64_t)gm.page_cost;
+    if (C >= L1) break;
+    const uint64_t pages = (rq.ctx_len + gm.page_tokens - 1) / gm.page_tokens;
+    if (C + pages * c <= L0) continue;
+    const uint64_t jb = L0 > C ? (L0 - C + c - 1) / c : 0;
+    const uint64_t je = min(pages, (L1 - C + c - 1) / c);
+    if (jb >= je) continue;
+    Seg sg;
+    sg.pg_begin = (uint32_t)jb;
+    sg.pg_end = (uint32_t)je;
+    sg.slot = (uint32_t)(w - rq.chunk_pages);
+    for (uint32_t hb = 0; hb < rq.n_hblk; ++hb) {
+      sg.hblk = hb;
+      run_seg<MASK>(a, rq, sg, buf0, buf1, red);
+      __syncthreads();  // LDS reuse by the next segment
+    }
+  }
+}
+
+// Work loop shared by the decode kernels. Queue schedule: workgroups pull
 // unit indices from a device counter until the queue is empty; the last
 // workgroup to leave resets the counters for the next launch.
 template <uint32_t MASK>
 __device__ __forceinline__ void decode_loop(const DecodeArgs &a, char *buf0, char *buf1, float *red, uint32_t *next) {
-  if (!a.persistent) {
+  if (a.schedule == kSchedBalanced) {
+    run_balanced<MASK>(a, buf0, buf1, red);
+    return;
+  }
+  if (a.schedule == kSchedGrid) {
     run_unit<MASK>(a, blockIdx.x, buf0, buf1, red);
     return;
   }
@@ -354,19 +410,20 @@ __device__ __forceinline__ void decode_loop(const DecodeArgs &a, char *buf0, cha
 template <uint32_t MASK, int NW>
 __global__ __launch_bounds__(64 * NW) void decode_kernel(const DecodeArgs a) {
   constexpr int B = kernel_buf_bytes(MASK);
-  __shared__ __attribute__((aligned(16))) char buf0[B];
-  __shared__ __attribute__((aligned(16))) char buf1[(MASK >> 16) ? B : 16];
+  constexpr int B1 = (MASK >> 16) ? B : 16;
+  // one array, so that a ring of tiles may span both buffers
+  __shared__ __attribute__((aligned(16))) char kv[B + B1];
   __shared__ float red[kRedFloats];
   __shared__ uint32_t next;
-  decode_loop<MASK>(a, buf0, buf1, red, &next);
+  decode_loop<MASK>(a, kv, kv + B, red, &next);
 }
 
 constexpr uint32_t vbit(int v) { return 1u << v; }
 // The variant sets the host launches together: each single variant, and
 // the mixed MLA-16 / MQA-32 / GQA-8 batch.
 constexpr uint32_t kMixedSmall = vbit(kV8x2) | vbit(kM_MLA_G16) | vbit(kM_D128_G32);
-constexpr uint32_t kAll4 = 0xFFu | vbit(kM_MLA_G16) | vbit(kM_D128_G16) | vbit(kM_D128_G32) | vbit(kM_D128_G64) |
-                           vbit(kM_D128_G128);
+constexpr uint32_t kAll4 = 0xFFu | vbit(kM_MLA_G16) | vbit(kM_MLA_G32) | vbit(kM_D128_G16) | vbit(kM_D128_G32) |
+                           vbit(kM_D128_G64) | vbit(kM_D128_G128);
 
 // Picks the kernel instantiation that covers `mask`. Returns
 // hipErrorInvalidValue for a set no instantiation covers (the host keeps
@@ -380,7 +437,7 @@ hipError_t launch_decode(const DecodeArgs &a, int grid, uint32_t mask, hipStream
   switch (mask) {
     CP_L(vbit(kV16x8), 4) CP_L(vbit(kV16x4), 4) CP_L(vbit(kV16x2), 4) CP_L(vbit(kV16x1), 4)
     CP_L(vbit(kV8x8), 4) CP_L(vbit(kV8x4), 4) CP_L(vbit(kV8x2), 4) CP_L(vbit(kV8x1), 4)
-    CP_L(vbit(kM_MLA_G16), 4) CP_L(vbit(kM_MLA_G32), 2) CP_L(vbit(kM_MLA_G128), 8)
+    CP_L(vbit(kM_MLA_G16), 4) CP_L(vbit(kM_MLA_G32), 4) CP_L(vbit(kM_MLA_G128), 8)
     CP_L(vbit(kM_D128_G16), 4) CP_L(vbit(kM_D128_G32), 4) CP_L(vbit(kM_D128_G64), 4) CP_L(vbit(kM_D128_G128), 4)
     CP_L(kMixedSmall, 4)
     default: break;
@@ -419,47 +476,95 @@ int decode_wgs_per_cu(uint32_t mask) {
 
 // ------------------------------------------------------------- merge
 
-// One wave per (split request, query head). Partials are folded in range
-// order with a running maximum, which equals
+// Split merge. One workgroup per (split request, query head, block of 128
+// V columns). First every thread takes some partials' lse values and the
+// block finds M = max_c lse_c; then wave w folds partials c = w, w+4, ...
+// with weights exp(lse_c - M) into its accumulators, and the four wave sums
+// are added in wave order:
 //   lse = M + ln sum_c exp(lse_c - M),  o = sum_c exp(lse_c - lse) o_c.
-__global__ __launch_bounds__(64) void merge_kernel(const MergeArgs a) {
-  const uint32_t row = blockIdx.x;
+__global__ __launch_bounds__(256) void merge_kernel(const MergeArgs a) {
+  __shared__ float red[4];
+  __shared__ float part[3][128];
+  const uint32_t nblk_total = blockIdx.x;
   int r = 0;
-  while (r + 1 < a.n_req && a.req[r + 1].head_begin <= row) ++r;
+  while (r + 1 < a.n_req && a.req[r + 1].block_begin <= nblk_total) ++r;
   const MergeReq &rq = a.req[r];
-  const uint32_t h = row - rq.head_begin;
-  const int lane = threadIdx.x;
-  const uint32_t dv = rq.d_v;
-  const int per = (int)dv / 64;  // 1, 2, 4 or 8
-  float acc[8];
-#pragma unroll
-  for (int j = 0; j < 8; ++j) acc[j] = 0.f;
-  float m = -INFINITY, l = 0.f;
+  const uint32_t dblocks = rq.d_v / 128 ? rq.d_v / 128 : 1;
+  const uint32_t local = nblk_total - rq.block_begin;
+  const uint32_t h = local / dblocks, db = local % dblocks;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   constexpr float kLog2e = 1.4426950408889634f;
-  for (uint32_t c = 0; c < rq.n_chunks; ++c) {
-    const uint64_t prow = (uint64_t)rq.ws_base + (uint64_t)c * rq.hq + h;
-    const float x = a.ws_l[prow] * kLog2e;
-    const float mn = fmaxf(m, x);
-    const float alpha = fast_exp2(m - mn);
-    const float w = fast_exp2(x - mn);
-    l = l * alpha + w;
-    m = mn;
-    const float *src = a.ws_o + ((uint64_t)rq.ws_orow + (uint64_t)c * rq.hq + h) * dv + (uint64_t)lane * per;
+  const uint32_t n = rq.n_chunks;
+  const uint64_t lrow0 = (uint64_t)rq.ws_base + h;  // lse of chunk c at lrow0 + c * hq
+  // block maximum of the partial lse values (log2 domain)
+  float mx = -INFINITY;
+  for (uint32_t c = threadIdx.x; c < n; c += 256) mx = fmaxf(mx, a.ws_l[lrow0 + (uint64_t)c * rq.hq] * kLog2e);
+  mx = wave_max(mx);
+  if (lane == 0) red[wave] = mx;
+  __syncthreads();
+  const float M = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+  __syncthreads();
+  // weighted sums; this lane covers columns db*128 + 2*lane (+1) when d_v >= 128
+  const uint32_t dv = rq.d_v;
+  const uint32_t per = dv >= 128 ? 2 : dv / 64;  // floats per lane
+  const uint32_t d0 = db * 128 + lane * per;
+  float acc0 = 0.f, acc1 = 0.f, l = 0.f;
+  const float *obase = a.ws_o + ((uint64_t)rq.ws_orow + h) * dv + d0;
+  const uint64_t ostride = (uint64_t)rq.hq * dv;
+  uint32_t c = wave;
+  for (; c + 12 < n; c += 16) {
+    float w[4], x0[4], x1[4];
 #pragma unroll
-    for (int j = 0; j < 8; ++j)
-      if (j < per) acc[j] = acc[j] * alpha + w * src[j];
+    for (int u = 0; u < 4; ++u) {
+      const uint32_t cc = c + 4 * u;
+      w[u] = a.ws_l[lrow0 + (uint64_t)cc * rq.hq];
+      const float *src = obase + (uint64_t)cc * ostride;
+      x0[u] = src[0];
+      x1[u] = per > 1 ? src[1] : 0.f;
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const float wu = fast_exp2(w[u] * kLog2e - M);
+      l += wu;
+      acc0 = fmaf(wu, x0[u], acc0);
+      acc1 = fmaf(wu, x1[u], acc1);
+    }
   }
-  const float inv = 1.0f / l;
-  uint16_t *dst = a.out + rq.o_off + h * dv + (uint32_t)lane * per;
+  for (; c < n; c += 4) {
+    const float wu = fast_exp2(a.ws_l[lrow0 + (uint64_t)c * rq.hq] * kLog2e - M);
+    const float *src = obase + (uint64_t)c * ostride;
+    l += wu;
+    acc0 = fmaf(wu, src[0], acc0);
+    if (per > 1) acc1 = fmaf(wu, src[1], acc1);
+  }
+  // combine the four waves in order
+  if (wave > 0) {
+    part[wave - 1][2 * lane] = acc0;
+    part[wave - 1][2 * lane + 1] = acc1;
+    if (lane == 0) red[wave] = l;
+  }
+  __syncthreads();
+  if (wave == 0) {
+    float L = l;
 #pragma unroll
-  for (int j = 0; j < 8; ++j)
-    if (j < per) dst[j] = (uint16_t)f32_to_bf16(acc[j] * inv);
-  if (lane == 0) a.lse[rq.lse_off + h] = (m + fast_log2(l)) * kLn2;
+    for (int w2 = 1; w2 < 4; ++w2) {
+      acc0 += part[w2 - 1][2 * lane];
+      acc1 += part[w2 - 1][2 * lane + 1];
+      L += red[w2];
+    }
+    const float inv = 1.0f / L;
+    if (d0 < dv) {
+      uint16_t *dst = a.out + rq.o_off + h * dv + d0;
+      dst[0] = (uint16_t)f32_to_bf16(acc0 * inv);
+      if (per > 1) dst[1] = (uint16_t)f32_to_bf16(acc1 * inv);
+    }
+    if (lane == 0 && db == 0) a.lse[rq.lse_off + h] = (M + fast_log2(L)) * kLn2;
+  }
 }
 
 hipError_t launch_merge(const MergeArgs &a, hipStream_t stream) {
-  if (a.total_heads <= 0) return hipSuccess;
-  hipLaunchKernelGGL(merge_kernel, dim3(a.total_heads), dim3(64), 0, stream, a);
+  if (a.n_blocks <= 0) return hipSuccess;
+  hipLaunchKernelGGL(merge_kernel, dim3(a.n_blocks), dim3(256), 0, stream, a);
   return hipGetLastError();
 }
 

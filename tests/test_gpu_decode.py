@@ -88,29 +88,43 @@ def test_append_in_many_calls_matches_concatenation():
 
 # ------------------------------------------------------------ decode parity
 
-@pytest.mark.parametrize("persistent", [1, 0])
-@pytest.mark.parametrize("splits", [0, 1, 3])
+BAL, QUE, GRD = cpl.CP_SCHED_BALANCED, cpl.CP_SCHED_QUEUE, cpl.CP_SCHED_GRID
+SCHEDULES = [(BAL, 0), (QUE, 0), (QUE, 1), (QUE, 3), (GRD, 0), (GRD, 5)]
+
+
+@pytest.mark.parametrize("schedule,splits", SCHEDULES)
 @pytest.mark.parametrize("path", [cpl.CP_PATH_AUTO, cpl.CP_PATH_VALU])
-def test_tiny_mla_workload(persistent, splits, path):
+def test_tiny_mla_workload(schedule, splits, path):
     wl = make_workload(1)
     ld = load(wl)
     try:
-        ld.decode(num_splits=splits, persistent=persistent, path=path)
+        ld.decode(num_splits=splits, schedule=schedule, path=path)
         torch.cuda.synchronize()
-        compare(ld, {r: expected_for(wl, r) for r in range(4)}, f"cfg1 p{persistent} s{splits} path{path}")
+        compare(ld, {r: expected_for(wl, r) for r in range(4)}, f"cfg1 sched{schedule} s{splits} path{path}")
     finally:
         ld.close()
 
 
-@pytest.mark.parametrize("splits", [0, 1, 4, 64])
+@pytest.mark.parametrize("schedule,splits", [(BAL, 0), (QUE, 0), (QUE, 1), (QUE, 4), (QUE, 64), (GRD, 4)])
 @pytest.mark.parametrize("path", [cpl.CP_PATH_AUTO, cpl.CP_PATH_VALU])
-def test_ragged_mixed_batch(splits, path):
+def test_ragged_mixed_batch(schedule, splits, path):
     wl = custom(RAGGED, seed=7)
     ld = load(wl, interleave=23)
     try:
-        ld.decode(num_splits=splits, path=path)
+        ld.decode(num_splits=splits, schedule=schedule, path=path)
         torch.cuda.synchronize()
-        compare(ld, {r: expected_for(wl, r) for r in range(len(RAGGED))}, f"ragged s{splits} path{path}")
+        compare(ld, {r: expected_for(wl, r) for r in range(len(RAGGED))}, f"ragged sched{schedule} s{splits} path{path}")
+    finally:
+        ld.close()
+
+
+def test_balanced_schedule_rejects_forced_splits():
+    wl = custom([("mla16", 100)], seed=2)
+    ld = load(wl)
+    try:
+        with pytest.raises(cpl.CrossPoolError) as e:
+            ld.decode(num_splits=2, schedule=BAL)
+        assert e.value.status == cpl.CP_EINVAL
     finally:
         ld.close()
 
@@ -119,21 +133,20 @@ VARIANT_MODELS = [("mla16", 700), ("mla32", 333), ("mla128", 290), ("mqa16", 515
                   ("gqa128x2", 257), ("mqa128", 129), ("gqa32x4", 450), ("gqa8x8d64", 97)]
 
 
-@pytest.mark.parametrize("splits", [0, 1, 5])
-@pytest.mark.parametrize("persistent", [1, 0])
-def test_every_kernel_variant(splits, persistent):
+@pytest.mark.parametrize("schedule,splits", SCHEDULES)
+def test_every_kernel_variant(schedule, splits):
     """One request per geometry, so every matrix-core and vector variant runs
     (workgroups of 2, 4 and 8 waves in separate launches of one call)."""
     wl = custom(VARIANT_MODELS, seed=41)
     ld = load(wl, interleave=31)
     try:
-        ld.decode(num_splits=splits, persistent=persistent)
+        ld.decode(num_splits=splits, schedule=schedule)
         torch.cuda.synchronize()
-        compare(ld, {r: expected_for(wl, r) for r in range(len(VARIANT_MODELS))}, f"variants s{splits} p{persistent}")
+        compare(ld, {r: expected_for(wl, r) for r in range(len(VARIANT_MODELS))}, f"variants sched{schedule} s{splits}")
         # the vector path on the same data agrees too
-        ld.decode(num_splits=splits, persistent=persistent, path=cpl.CP_PATH_VALU)
+        ld.decode(num_splits=splits, schedule=schedule, path=cpl.CP_PATH_VALU)
         torch.cuda.synchronize()
-        compare(ld, {r: expected_for(wl, r) for r in range(len(VARIANT_MODELS))}, f"variants vector s{splits}")
+        compare(ld, {r: expected_for(wl, r) for r in range(len(VARIANT_MODELS))}, f"variants vector sched{schedule}")
     finally:
         ld.close()
 
@@ -210,13 +223,13 @@ def test_split_and_unsplit_agree():
     wl = custom([("mla16", 5000), ("gqa32x4", 4100), ("mqa32", 2300)], seed=31)
     ld = load(wl)
     try:
-        ld.decode(num_splits=1)
+        ld.decode(num_splits=1, schedule=QUE)
         torch.cuda.synchronize()
         a = ld.out.clone()
         exp = {r: expected_for(wl, r) for r in range(3)}
         compare(ld, exp, "unsplit")
         for k in (2, 7, 40):
-            ld.decode(num_splits=k)
+            ld.decode(num_splits=k, schedule=QUE)
             torch.cuda.synchronize()
             compare(ld, exp, f"split{k}")
         d = (a.view(torch.bfloat16).float() - ld.out.view(torch.bfloat16).float()).abs().max().item()
