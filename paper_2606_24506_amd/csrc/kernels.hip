@@ -65,11 +65,15 @@ hipError_t launch_gather(const GatherArgs &a, hipStream_t stream) {
 
 // ------------------------------------------------- decode: vector path
 
-// Loads DPL consecutive bf16 values as floats.
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x2_t __attribute__((ext_vector_type(2)));
+
+// Loads DPL consecutive bf16 values of streamed KV as floats (non-temporal:
+// KV is read once per call).
 template <int DPL>
 CP_DEV void load_bf16(const uint8_t *p, float (&v)[DPL]) {
   if constexpr (DPL == 8) {
-    uint4 w = *reinterpret_cast<const uint4 *>(p);
+    const u32x4_t w = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t *>(p));
     uint32_t x[4] = {w.x, w.y, w.z, w.w};
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
@@ -77,13 +81,13 @@ CP_DEV void load_bf16(const uint8_t *p, float (&v)[DPL]) {
       v[2 * i + 1] = __uint_as_float(x[i] & 0xffff0000u);
     }
   } else if constexpr (DPL == 4) {
-    uint2 w = *reinterpret_cast<const uint2 *>(p);
+    const u32x2_t w = __builtin_nontemporal_load(reinterpret_cast<const u32x2_t *>(p));
     v[0] = __uint_as_float(w.x << 16);
     v[1] = __uint_as_float(w.x & 0xffff0000u);
     v[2] = __uint_as_float(w.y << 16);
     v[3] = __uint_as_float(w.y & 0xffff0000u);
   } else if constexpr (DPL == 2) {
-    uint32_t w = *reinterpret_cast<const uint32_t *>(p);
+    const uint32_t w = __builtin_nontemporal_load(reinterpret_cast<const uint32_t *>(p));
     v[0] = __uint_as_float(w << 16);
     v[1] = __uint_as_float(w & 0xffff0000u);
   } else {
