@@ -18,10 +18,13 @@ HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 DEVICE_FLAGS = ["--offload-arch=gfx950", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
 # Matrix-core accumulators stay in architectural VGPRs: the decode loops
 # rescale them with vector ops, and AGPR homes would cost a copy each way.
+# Where a kernel needs more than 256 registers (the 128-head MLA path), the
+# register allocator parks long-lived operands in the accumulation registers
+# instead of scratch memory.
 KERNEL_FLAGS = ["-mllvm", "-amdgpu-mfma-vgpr-form"]
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-function", f"-I{os.path.join(ROOT, 'include')}", f"-I{CSRC}"]
 
-SOURCES = ["api.cpp", "pool.cpp", "kernels.hip"]
+SOURCES = ["api.cpp", "pool.cpp", "kernels.hip", "wide_kernels.hip"]
 
 
 def _run(cmd):

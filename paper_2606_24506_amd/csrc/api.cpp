@@ -18,7 +18,7 @@ namespace cp {
 hipError_t launch_append(const AppendArgs &a, hipStream_t stream);
 hipError_t launch_gather(const GatherArgs &a, hipStream_t stream);
 hipError_t launch_decode(const DecodeArgs &a, int grid, uint32_t mask, hipStream_t stream);
-int decode_waves(int variant);
+hipError_t launch_decode_wide(const DecodeArgs &a, int grid, int variant, hipStream_t stream);
 int decode_wgs_per_cu(uint32_t mask);
 hipError_t launch_merge(const MergeArgs &a, hipStream_t stream);
 }  // namespace cp
@@ -517,7 +517,12 @@ cp_status cp_attn_decode_ex(cp_pool *p, int32_t n, const int32_t *req_ids, const
   }
   if (qo > 0xFFFFFFFFull || oo > 0xFFFFFFFFull) return fail(CP_EINVAL, "batch too large");
   auto model_of = [&](int32_t i) { return p->st.req(req_ids[i]).model; };
-  auto wclass = [&](int32_t i) { return decode_waves(gk[model_of(i)].variant); };
+  // kernel family: the narrow kernel covers every vector and narrow matrix
+  // variant in one launch; each wide variant has a kernel of its own
+  auto wclass = [&](int32_t i) {
+    const int v = gk[model_of(i)].variant;
+    return is_wide_variant(v) ? v : 0;
+  };
 
   // Launch groups: requests whose kernels share a workgroup size, at most
   // kMaxReqPerLaunch requests and kMaxLaunchModels models each. Within the
@@ -557,7 +562,8 @@ cp_status cp_attn_decode_ex(cp_pool *p, int32_t n, const int32_t *req_ids, const
     hblk[i] = g.hkv * gk[model_of(i)].nb;
   }
   for (Group &g : groups) {
-    const int wgs = decode_wgs_per_cu(g.mask);
+    const bool wide = g.mask && is_wide_variant(__builtin_ctz(g.mask));
+    const int wgs = wide ? 1 : decode_wgs_per_cu(g.mask);
     const int64_t slots = (int64_t)p->num_cus * wgs;
     if (o.schedule == CP_SCHED_BALANCED) {
       uint64_t T = 0, maxc = 1;
@@ -590,7 +596,7 @@ cp_status cp_attn_decode_ex(cp_pool *p, int32_t n, const int32_t *req_ids, const
       std::vector<int32_t> hb;
       for (int32_t i : g.idx) {
         const int32_t v = gk[model_of(i)].variant;
-        all_wide = all_wide && (v == 18 || v == 22);
+        all_wide = all_wide && is_wide_variant(v);
         any_matrix = any_matrix || v >= kMatrixFirst;
         pin.push_back(PlanIn{model_of(i), p->st.req(req_ids[i]).ctx_len});
         hb.push_back(hblk[i]);
@@ -678,7 +684,8 @@ cp_status cp_attn_decode_ex(cp_pool *p, int32_t n, const int32_t *req_ids, const
       d.n_hblk = (uint16_t)hblk[i];
     }
     if (g.grid > 0xFFFF && o.schedule == CP_SCHED_BALANCED) return fail(CP_EINVAL, "too many workers");
-    hipError_t e = launch_decode(a, g.grid, g.mask, s);
+    const int v0 = __builtin_ctz(g.mask);
+    hipError_t e = is_wide_variant(v0) ? launch_decode_wide(a, g.grid, v0, s) : launch_decode(a, g.grid, g.mask, s);
     if (e != hipSuccess) return hip_fail(e, "decode launch");
   }
   if (o.ev_end) {

@@ -13,6 +13,7 @@
 #include "decode_mfma.h"
 #include "device_common.h"
 #include "kargs.h"
+#include "schedule.h"
 
 namespace cp {
 
@@ -254,25 +255,11 @@ __device__ __forceinline__ void valu_unit(const DecodeArgs &a, const GeomK &gm, 
   __syncthreads();  // LDS is reused by the next unit
 }
 
-// Code-path variants (GeomK::variant). Vector path (ids 0-7): heads per
-// block and V elements per lane. Matrix path (ids 16-22): head blocks per
-// wave, waves per tile, waves per workgroup, K width, V width, tile tokens.
-enum : int32_t {
-  kV16x8 = 0, kV16x4, kV16x2, kV16x1, kV8x8, kV8x4, kV8x2, kV8x1,
-  kM_MLA_G16 = 16, kM_MLA_G32, kM_MLA_G128, kM_D128_G16, kM_D128_G32, kM_D128_G64, kM_D128_G128
-};
-
 template <int V> struct Mcfg;
 template <> struct Mcfg<kM_MLA_G16> { using C = CoopCfg<1, 576, 512, true, 2, 3>; };
 template <> struct Mcfg<kM_MLA_G32> { using C = CoopCfg<2, 576, 512, true, 2, 3>; };
-template <> struct Mcfg<kM_MLA_G128> { using C = MfmaCfg<1, 8, 8, 576, 512, 32, true>; };
 template <> struct Mcfg<kM_D128_G16> { using C = CoopCfg<1, 128, 128, false, 4, 3>; };
 template <> struct Mcfg<kM_D128_G32> { using C = CoopCfg<2, 128, 128, false, 4, 3>; };
-template <> struct Mcfg<kM_D128_G64> { using C = MfmaCfg<4, 1, 4, 128, 128, 32, false>; };
-template <> struct Mcfg<kM_D128_G128> { using C = MfmaCfg<2, 4, 4, 128, 128, 32, false>; };
-
-// Waves per workgroup of each variant (vector variants use four).
-constexpr int variant_waves(int v) { return v == kM_MLA_G128 ? 8 : 4; }
 
 template <int V>
 constexpr int mcfg_buf() { return Mcfg<V>::C::BUF; }
@@ -284,8 +271,7 @@ constexpr int kernel_buf_bytes(uint32_t mask) {
   int b = 0;
   if (mask & 0xFFu) b = kLdsFloats * 4 > b ? kLdsFloats * 4 : b;
 #define CP_B(V) if (has(mask, V) && mcfg_buf<V>() > b) b = mcfg_buf<V>();
-  CP_B(kM_MLA_G16) CP_B(kM_MLA_G32) CP_B(kM_MLA_G128) CP_B(kM_D128_G16) CP_B(kM_D128_G32) CP_B(kM_D128_G64)
-  CP_B(kM_D128_G128)
+  CP_B(kM_MLA_G16) CP_B(kM_MLA_G32) CP_B(kM_D128_G16) CP_B(kM_D128_G32)
 #undef CP_B
   return b;
 }
@@ -305,13 +291,6 @@ __device__ __forceinline__ void run_seg(const DecodeArgs &a, const DecReq &rq, c
   CP_VCASE(kV16x8, 16, 8) CP_VCASE(kV16x4, 16, 4) CP_VCASE(kV16x2, 16, 2) CP_VCASE(kV16x1, 16, 1)
   CP_VCASE(kV8x8, 8, 8) CP_VCASE(kV8x4, 8, 4) CP_VCASE(kV8x2, 8, 2) CP_VCASE(kV8x1, 8, 1)
 #undef CP_VCASE
-#define CP_MCASE(V, HBW, WPT, NW, DK, DV, T, MLA)                                    \
-  if constexpr (has(MASK, V)) {                                                      \
-    if (gm.variant == V) {                                                           \
-      mfma_unit<HBW, WPT, NW, DK, DV, T, MLA>(a, gm, rq, sg, buf0, buf1, red);       \
-      return;                                                                        \
-    }                                                                                \
-  }
 #define CP_CCASE(V, HBW, DK, DV, MLA, NS, NBUF)                                      \
   if constexpr (has(MASK, V)) {                                                      \
     if (gm.variant == V) {                                                           \
@@ -324,137 +303,50 @@ __device__ __forceinline__ void run_seg(const DecodeArgs &a, const DecReq &rq, c
   CP_CCASE(kM_D128_G16, 1, 128, 128, false, 4, 3)
   CP_CCASE(kM_D128_G32, 2, 128, 128, false, 4, 3)
 #undef CP_CCASE
-  CP_MCASE(kM_MLA_G128, 1, 8, 8, 576, 512, 32, true)
-  CP_MCASE(kM_D128_G64, 4, 1, 4, 128, 128, 32, false)
-  CP_MCASE(kM_D128_G128, 2, 4, 4, 128, 128, 32, false)
-#undef CP_MCASE
 }
 
-// Queue and grid schedules: unit u is (request, KV range, head block).
+// One kernel per variant set of the narrow family; four waves per
+// workgroup, two KV buffers sized for the largest variant in the set.
 template <uint32_t MASK>
-__device__ __forceinline__ void run_unit(const DecodeArgs &a, uint32_t u, char *buf0, char *buf1, float *red) {
-  int r = 0;
-  while (r + 1 < a.n_req && a.req[r + 1].unit_begin <= u) ++r;
-  const DecReq &rq = a.req[r];
-  const uint32_t local = u - rq.unit_begin;
-  const uint32_t chunk = local / rq.n_hblk;
-  const uint32_t pages = (rq.ctx_len + a.geom[rq.model].page_tokens - 1) / a.geom[rq.model].page_tokens;
-  Seg sg;
-  sg.pg_begin = chunk * rq.chunk_pages;
-  sg.pg_end = min(pages, sg.pg_begin + rq.chunk_pages);
-  sg.slot = chunk;
-  sg.hblk = local % rq.n_hblk;
-  run_seg<MASK>(a, rq, sg, buf0, buf1, red);
-}
-
-// Balanced schedule. The launch's requests, in order, form one sequence of
-// pages; page j of request r covers costs [C_r + j c_r, C_r + (j+1) c_r)
-// with C_r the cost prefix and c_r its model's page cost. Workgroup w owns
-// the pages whose first cost lies in [w T / W, (w+1) T / W) (T the total
-// cost, W the grid), so every workgroup gets the same work to within one
-// page. Its pages of request r land in partial slot w - w_first(r).
-template <uint32_t MASK>
-__device__ __forceinline__ void run_balanced(const DecodeArgs &a, char *buf0, char *buf1, float *red) {
-  const uint64_t W = gridDim.x, w = blockIdx.x, T = a.total_cost;
-  const uint64_t L0 = w * T / W, L1 = (w + 1) * T / W;
-  for (int r = 0; r < a.n_req; ++r) {
-    const DecReq &rq = a.req[r];
-    const GeomK &gm = a.geom[rq.model];
-    const uint64_t C = rq.unit_begin, c = (uint64_t)gm.page_cost;
-    if (C >= L1) break;
-    const uint64_t pages = (rq.ctx_len + gm.page_tokens - 1) / gm.page_tokens;
-    if (C + pages * c <= L0) continue;
-    const uint64_t jb = L0 > C ? (L0 - C + c - 1) / c : 0;
-    const uint64_t je = min(pages, (L1 - C + c - 1) / c);
-    if (jb >= je) continue;
-    Seg sg;
-    sg.pg_begin = (uint32_t)jb;
-    sg.pg_end = (uint32_t)je;
-    sg.slot = (uint32_t)(w - rq.chunk_pages);
-    for (uint32_t hb = 0; hb < rq.n_hblk; ++hb) {
-      sg.hblk = hb;
-      run_seg<MASK>(a, rq, sg, buf0, buf1, red);
-      __syncthreads();  // LDS reuse by the next segment
-    }
-  }
-}
-
-// Work loop shared by the decode kernels. Queue schedule: workgroups pull
-// unit indices from a device counter until the queue is empty; the last
-// workgroup to leave resets the counters for the next launch.
-template <uint32_t MASK>
-__device__ __forceinline__ void decode_loop(const DecodeArgs &a, char *buf0, char *buf1, float *red, uint32_t *next) {
-  if (a.schedule == kSchedBalanced) {
-    run_balanced<MASK>(a, buf0, buf1, red);
-    return;
-  }
-  if (a.schedule == kSchedGrid) {
-    run_unit<MASK>(a, blockIdx.x, buf0, buf1, red);
-    return;
-  }
-  for (;;) {
-    if (threadIdx.x == 0) *next = atomicAdd(&a.queue[0], 1u);
-    __syncthreads();
-    const uint32_t u = *next;
-    __syncthreads();
-    if (u >= (uint32_t)a.n_units) break;
-    run_unit<MASK>(a, u, buf0, buf1, red);
-  }
-  if (threadIdx.x == 0) {
-    __threadfence();
-    if (atomicAdd(&a.queue[1], 1u) == gridDim.x - 1) {
-      atomicExch(&a.queue[0], 0u);
-      atomicExch(&a.queue[1], 0u);
-    }
-  }
-}
-
-// One kernel per variant set; NW waves per workgroup, two KV buffers sized
-// for the largest variant in the set.
-template <uint32_t MASK, int NW>
-__global__ __launch_bounds__(64 * NW) void decode_kernel(const DecodeArgs a) {
+__global__ __launch_bounds__(256) void decode_kernel(const DecodeArgs a) {
   constexpr int B = kernel_buf_bytes(MASK);
   constexpr int B1 = (MASK >> 16) ? B : 16;
   // one array, so that a ring of tiles may span both buffers
   __shared__ __attribute__((aligned(16))) char kv[B + B1];
   __shared__ float red[kRedFloats];
   __shared__ uint32_t next;
-  decode_loop<MASK>(a, kv, kv + B, red, &next);
+  decode_loop(a, &next, [&](const DecReq &rq, const Seg &sg) { run_seg<MASK>(a, rq, sg, kv, kv + B, red); });
 }
 
 constexpr uint32_t vbit(int v) { return 1u << v; }
 // The variant sets the host launches together: each single variant, and
 // the mixed MLA-16 / MQA-32 / GQA-8 batch.
 constexpr uint32_t kMixedSmall = vbit(kV8x2) | vbit(kM_MLA_G16) | vbit(kM_D128_G32);
-constexpr uint32_t kAll4 = 0xFFu | vbit(kM_MLA_G16) | vbit(kM_MLA_G32) | vbit(kM_D128_G16) | vbit(kM_D128_G32) |
-                           vbit(kM_D128_G64) | vbit(kM_D128_G128);
+constexpr uint32_t kAll4 = 0xFFu | vbit(kM_MLA_G16) | vbit(kM_MLA_G32) | vbit(kM_D128_G16) | vbit(kM_D128_G32);
 
 // Picks the kernel instantiation that covers `mask`. Returns
 // hipErrorInvalidValue for a set no instantiation covers (the host keeps
 // variants of different workgroup sizes in separate launches).
 hipError_t launch_decode(const DecodeArgs &a, int grid, uint32_t mask, hipStream_t stream) {
   const dim3 g(grid);
-#define CP_L(M, NW)                                                                   \
+#define CP_L(M)                                                                       \
   case M:                                                                             \
-    hipLaunchKernelGGL((decode_kernel<M, NW>), g, dim3(64 * NW), 0, stream, a);       \
+    hipLaunchKernelGGL((decode_kernel<M>), g, dim3(256), 0, stream, a);               \
     return hipGetLastError();
   switch (mask) {
-    CP_L(vbit(kV16x8), 4) CP_L(vbit(kV16x4), 4) CP_L(vbit(kV16x2), 4) CP_L(vbit(kV16x1), 4)
-    CP_L(vbit(kV8x8), 4) CP_L(vbit(kV8x4), 4) CP_L(vbit(kV8x2), 4) CP_L(vbit(kV8x1), 4)
-    CP_L(vbit(kM_MLA_G16), 4) CP_L(vbit(kM_MLA_G32), 4) CP_L(vbit(kM_MLA_G128), 8)
-    CP_L(vbit(kM_D128_G16), 4) CP_L(vbit(kM_D128_G32), 4) CP_L(vbit(kM_D128_G64), 4) CP_L(vbit(kM_D128_G128), 4)
-    CP_L(kMixedSmall, 4)
+    CP_L(vbit(kV16x8)) CP_L(vbit(kV16x4)) CP_L(vbit(kV16x2)) CP_L(vbit(kV16x1))
+    CP_L(vbit(kV8x8)) CP_L(vbit(kV8x4)) CP_L(vbit(kV8x2)) CP_L(vbit(kV8x1))
+    CP_L(vbit(kM_MLA_G16)) CP_L(vbit(kM_MLA_G32)) CP_L(vbit(kM_D128_G16)) CP_L(vbit(kM_D128_G32))
+    CP_L(kMixedSmall)
     default: break;
   }
 #undef CP_L
   if ((mask & ~kAll4) == 0) {
-    hipLaunchKernelGGL((decode_kernel<kAll4, 4>), g, dim3(256), 0, stream, a);
+    hipLaunchKernelGGL((decode_kernel<kAll4>), g, dim3(256), 0, stream, a);
     return hipGetLastError();
   }
   return hipErrorInvalidValue;
 }
-
-int decode_waves(int variant) { return variant_waves(variant); }
 
 // Workgroups of one kernel that fit on a CU at once (LDS-bound).
 int decode_wgs_per_cu(uint32_t mask) {
@@ -465,11 +357,8 @@ int decode_wgs_per_cu(uint32_t mask) {
     switch (v) {
       case kM_MLA_G16: bytes = 2 * mcfg_buf<kM_MLA_G16>(); break;
       case kM_MLA_G32: bytes = 2 * mcfg_buf<kM_MLA_G32>(); break;
-      case kM_MLA_G128: bytes = 2 * mcfg_buf<kM_MLA_G128>(); break;
       case kM_D128_G16: bytes = 2 * mcfg_buf<kM_D128_G16>(); break;
       case kM_D128_G32: bytes = 2 * mcfg_buf<kM_D128_G32>(); break;
-      case kM_D128_G64: bytes = 2 * mcfg_buf<kM_D128_G64>(); break;
-      case kM_D128_G128: bytes = 2 * mcfg_buf<kM_D128_G128>(); break;
       default: bytes = kLdsFloats * 4; break;
     }
     b = bytes > b ? bytes : b;

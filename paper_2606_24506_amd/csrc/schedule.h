@@ -1,0 +1,94 @@
+// Work distribution shared by the decode kernels. A decode launch covers
+// several requests (possibly of different models); `seg(rq, sg)` runs one
+// piece of work: pages [sg.pg_begin, sg.pg_end) of request rq for KV head
+// (or head block) sg.hblk, writing partial slot sg.slot when the request is
+// split.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include "kargs.h"
+
+namespace cp {
+
+// Finds the next piece of work of this workgroup for the balanced
+// schedule, starting the search at request *r, head block *hb. Returns
+// false when the workgroup's share is exhausted.
+__device__ __forceinline__ bool next_balanced(const DecodeArgs &a, int *r, uint32_t *hb, Seg *sg) {
+  const uint64_t W = gridDim.x, w = blockIdx.x, T = a.total_cost;
+  const uint64_t L0 = w * T / W, L1 = (w + 1) * T / W;
+  for (; *r < a.n_req; ++*r, *hb = 0) {
+    const DecReq &rq = a.req[*r];
+    const GeomK &gm = a.geom[rq.model];
+    const uint64_t C = rq.unit_begin, c = (uint64_t)gm.page_cost;
+    if (C >= L1) return false;
+    const uint64_t pages = (rq.ctx_len + gm.page_tokens - 1) / gm.page_tokens;
+    if (C + pages * c <= L0) continue;
+    const uint64_t jb = L0 > C ? (L0 - C + c - 1) / c : 0;
+    const uint64_t je = min(pages, (L1 - C + c - 1) / c);
+    if (jb >= je || *hb >= rq.n_hblk) continue;
+    sg->pg_begin = (uint32_t)jb;
+    sg->pg_end = (uint32_t)je;
+    sg->slot = (uint32_t)(w - rq.chunk_pages);
+    sg->hblk = *hb;
+    return true;
+  }
+  return false;
+}
+
+// Decodes unit u of the queue and grid schedules into (request, piece).
+__device__ __forceinline__ int unit_segment(const DecodeArgs &a, uint32_t u, Seg *sg) {
+  int r = 0;
+  while (r + 1 < a.n_req && a.req[r + 1].unit_begin <= u) ++r;
+  const DecReq &rq = a.req[r];
+  const uint32_t local = u - rq.unit_begin;
+  const uint32_t chunk = local / rq.n_hblk;
+  const uint32_t pages = (rq.ctx_len + a.geom[rq.model].page_tokens - 1) / a.geom[rq.model].page_tokens;
+  sg->pg_begin = chunk * rq.chunk_pages;
+  sg->pg_end = min(pages, sg->pg_begin + rq.chunk_pages);
+  sg->slot = chunk;
+  sg->hblk = local % rq.n_hblk;
+  return r;
+}
+
+// Work loop of every decode kernel; `seg` is inlined once. Queue schedule:
+// workgroups pull unit indices from a device counter until the queue is
+// empty; the last workgroup to leave resets the counters for the next
+// launch.
+template <class F>
+__device__ __forceinline__ void decode_loop(const DecodeArgs &a, uint32_t *next, F &&seg) {
+  int br = 0;        // balanced: request being searched
+  uint32_t bhb = 0;  // balanced: next head block of that request
+  bool first = true;
+  for (;;) {
+    Seg sg;
+    int r;
+    if (a.schedule == kSchedBalanced) {
+      if (!next_balanced(a, &br, &bhb, &sg)) break;
+      r = br;
+      ++bhb;
+    } else if (a.schedule == kSchedGrid) {
+      if (!first) break;
+      r = unit_segment(a, blockIdx.x, &sg);
+    } else {
+      if (threadIdx.x == 0) *next = atomicAdd(&a.queue[0], 1u);
+      __syncthreads();
+      const uint32_t u = *next;
+      __syncthreads();
+      if (u >= (uint32_t)a.n_units) break;
+      r = unit_segment(a, u, &sg);
+    }
+    first = false;
+    seg(a.req[r], sg);
+    __syncthreads();  // LDS reuse by the next piece
+  }
+  if (a.schedule == kSchedQueue && threadIdx.x == 0) {
+    __threadfence();
+    if (atomicAdd(&a.queue[1], 1u) == gridDim.x - 1) {
+      atomicExch(&a.queue[0], 0u);
+      atomicExch(&a.queue[1], 0u);
+    }
+  }
+}
+
+}  // namespace cp
