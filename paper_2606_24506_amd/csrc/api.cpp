@@ -407,25 +407,37 @@ void choose_valu(const Geom &g, GeomK *k) {
 constexpr int32_t kMatrixFirst = 16;
 
 // Matrix-core variant for a model, or -1 when none fits its geometry. The
-// matrix path is used where at least 16 query heads share one KV head, so
-// the per-KV-head work is a dense contraction (MLA latent head, MQA, wide
-// GQA groups). The 16- and 32-head variants tile whole 64-token pages; the
-// wider ones need page_tokens to be a multiple of 32.
+// matrix path serves models whose query heads share a KV head in groups of
+// 8 or more (the MLA latent head, MQA, GQA), where the per-KV-head work is a
+// contraction over the group: the narrow variants (8-32 heads) stream
+// wave-private slices of 16 (MLA) or 32 (head_dim 128) tokens, the wide ones
+// (64-128 heads) 32-token tiles shared by the workgroup. Pages must hold a
+// whole number of slices or tiles.
 int32_t matrix_variant(const Geom &g, int32_t P) {
-  if (P % 32) return -1;
   if (g.kind == kMLA && g.latent == 512 && g.rope == 64) {
-    if (g.g == 16 && P == 64) return 16;
-    if (g.g == 32 && P == 64) return 17;
-    if (g.g == 128) return 18;
+    if (g.g == 16 && P % 16 == 0) return kM_MLA_G16;
+    if (g.g == 32 && P % 16 == 0) return kM_MLA_G32;
+    if (g.g == 128 && P % 32 == 0) return kM_MLA_G128;
     return -1;
   }
-  if (g.kind == kGQA && g.head_dim == 128) {
-    if (g.g == 16 && P == 64) return 19;
-    if (g.g == 32 && P == 64) return 20;
-    if (g.g == 64) return 21;
-    if (g.g == 128) return 22;
+  if (g.kind == kGQA && g.head_dim == 128 && P % 32 == 0) {
+    if (g.g == 8) return kM_D128_G8;
+    if (g.g == 16) return kM_D128_G16;
+    if (g.g == 32) return kM_D128_G32;
+    if (g.g == 64) return kM_D128_G64;
+    if (g.g == 128) return kM_D128_G128;
   }
   return -1;
+}
+
+// Work units per KV range of a request: the narrow matrix kernel takes four
+// KV heads at once (one per wave) when the model has a multiple of four;
+// otherwise every KV head (times its head blocks on the vector path) is a
+// unit of its own.
+int32_t units_per_range(const Geom &g, const GeomK &k) {
+  const bool narrow = k.variant >= kMatrixFirst && !is_wide_variant(k.variant);
+  if (narrow && g.hkv % 4 == 0) return g.hkv / 4;
+  return g.hkv * k.nb;
 }
 
 cp_status ensure_ws(cp_pool *p, uint64_t o_floats, uint64_t l_floats) {
@@ -485,7 +497,7 @@ cp_status cp_attn_decode_ex(cp_pool *p, int32_t n, const int32_t *req_ids, const
     const int32_t mv = o.path == CP_PATH_VALU ? -1 : matrix_variant(g, P);
     if (mv >= 0) {
       gk[m].variant = mv;
-      gk[m].nb = 1;
+      gk[m].nb = mv == kM_MLA_G32 ? 2 : 1;  // units of 16 heads per KV range
     } else {
       choose_valu(g, &gk[m]);
     }
@@ -497,7 +509,7 @@ cp_status cp_attn_decode_ex(cp_pool *p, int32_t n, const int32_t *req_ids, const
   for (int32_t i = 0; i < n; ++i) {
     const int32_t m = p->st.req(req_ids[i]).model;
     if (o.path == CP_PATH_MFMA && gk[m].variant < kMatrixFirst)
-      return fail(CP_EINVAL, "model %d has no matrix-core variant (needs >= 16 query heads per KV head)", m);
+      return fail(CP_EINVAL, "model %d has no matrix-core variant (needs a group of 8, 16, 32, 64 or 128 query heads per KV head)", m);
   }
 
   // Packed offsets in call order.
@@ -559,7 +571,7 @@ cp_status cp_attn_decode_ex(cp_pool *p, int32_t n, const int32_t *req_ids, const
   std::vector<uint32_t> cost_prefix(n, 0);
   for (int32_t i = 0; i < n; ++i) {
     const Geom &g = p->st.model(model_of(i));
-    hblk[i] = g.hkv * gk[model_of(i)].nb;
+    hblk[i] = units_per_range(g, gk[model_of(i)]);
   }
   for (Group &g : groups) {
     const bool wide = g.mask && is_wide_variant(__builtin_ctz(g.mask));

@@ -52,6 +52,7 @@ struct WideCfg {
   static constexpr int HBQ = G / 64;                 // head blocks each wave scores
   static constexpr int DBW = DV / 64;                // V column blocks each wave accumulates
   static constexpr int QR = KSTEPS - QL;             // query k-steps held in registers
+  static constexpr bool AGPR_Q = HB * DBW * 4 >= 192;  // accumulators fill the architectural file
   static constexpr int PBYTES = HB * 64 * 16;        // P^T fragments of one tile
   static constexpr int QBYTES = 4 * HBQ * QL * 1024; // query fragments kept in LDS
   static constexpr int XBYTES = 16 + G * 4 * 2;      // flags, rescale factors, final m / l
@@ -72,7 +73,8 @@ __device__ __forceinline__ void wide_unit(const DecodeArgs &a, const GeomK &gm, 
                                           char *lds) {
   using C = WideCfg<G, DK, DV, MLA, QL>;
   const uint32_t kvh = sg.hblk, slot = sg.slot;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // uniform: lets wave-derived values live in SGPRs
   const int col = lane & 15, quad = lane >> 4;
   const int P = gm.page_tokens;  // the host routes only pages of a multiple of 32 tokens here
   const int tpp = P / C::T;        // tiles per page
@@ -94,7 +96,13 @@ __device__ __forceinline__ void wide_unit(const DecodeArgs &a, const GeomK &gm, 
   for (int hb = 0; hb < C::HBQ; ++hb) {
     const uint16_t *qrow = a.q + rq.q_off + (uint32_t)(h_kv + (G / 4) * wave + 16 * hb + col) * DK + 8 * quad;
 #pragma unroll
-    for (int c = 0; c < C::QR; ++c) qf[hb][c] = *reinterpret_cast<const bf16x8 *>(qrow + 32 * c);
+    for (int c = 0; c < C::QR; ++c) {
+      qf[hb][c] = *reinterpret_cast<const bf16x8 *>(qrow + 32 * c);
+      // the query lives in the accumulation registers, which the matrix
+      // cores read directly as their B operand; the P.V accumulators take
+      // the architectural registers
+      if constexpr (C::AGPR_Q) asm volatile("" : "+a"(qf[hb][c]));
+    }
 #pragma unroll
     for (int c = 0; c < QL; ++c)
       *reinterpret_cast<bf16x8 *>(qmine + ((hb * QL + c) * 64 + lane) * 16) =
@@ -115,40 +123,75 @@ __device__ __forceinline__ void wide_unit(const DecodeArgs &a, const GeomK &gm, 
     const int sp = batch * 64 + lane;
     pte_lane = sp < npg ? a.pte[rq.pte_base + pg_begin + (uint32_t)sp] : 0u;
     pte_batch = batch;
+    // Wait here, visibly to the compiler: the tile loads are inline asm it
+    // cannot count, so a wait it placed at the first use of pte_lane would
+    // be a full vmcnt(0) in every tile, draining the KV loads in flight.
+    // This drains them once per 64 pages instead.
+    __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
   };
-  // Direct loads of tile k into its ring slot: load i of the tile covers LDS
-  // bytes [1024 i, 1024 i + 1024) of the slot; wave w issues loads w, w+4, ...
-  // Lanes on a row's 16-byte pad refetch the row's first 16 bytes (same
-  // cache lines, never read back); lanes past the tile issue nothing.
-  auto issue = [&](int k) {
-    char *dst = ring + (k % C::NBUF) * C::TILE;
+  // Direct loads of a tile into its ring slot. Load i of the tile covers
+  // LDS bytes [1024 i, 1024 i + 1024) of the slot. Wave w issues a
+  // contiguous range of loads, in groups of up to four per M0 write
+  // (dma_group); the groups are spread over the tile's work so that an M0
+  // write rarely finds the previous group still queued. Lanes on a row's
+  // 16-byte pad fetch the row's last 16 bytes again (same cache line, never
+  // read back); lanes past the tile are masked off.
+  constexpr int LBASE = C::NLOADS / 4, LREM = C::NLOADS % 4;
+  constexpr int MY_MAX = LBASE + (LREM ? 1 : 0);  // loads of the busiest wave
+  constexpr int NGRP = (MY_MAX + 3) / 4;          // M0 groups per wave and tile
+  const int my_loads = LBASE + (wave < LREM ? 1 : 0);
+  const int my_first = wave * LBASE + min(wave, LREM);
+  // per-lane global offsets of this wave's loads, biased for dma_group
+  uint32_t voff[NGRP][4];
+#pragma unroll
+  for (int g = 0; g < NGRP; ++g)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int o = (my_first + 4 * g + j) * 1024 + lane * 16;
+      uint32_t gofs;
+      if (C::TILE_V == 0 || o < C::TILE_K) {
+        const int oc = o < C::TILE_K ? o : 0;
+        const int row = oc / C::KPITCH, w = oc - row * C::KPITCH;
+        gofs = (uint32_t)(row * C::KROW + (w < C::KROW ? w : C::KROW - 16));
+      } else {
+        const int o2 = o < C::TILE ? o - C::TILE_K : 0;
+        const int row = o2 / C::VPITCH, w = o2 - row * C::VPITCH;
+        gofs = (uint32_t)(P * DK * 2 + row * C::VROW + (w < C::VROW ? w : C::VROW - 16));
+      }
+      voff[g][j] = gofs + kDmaBias - 1024u * j;
+    }
+  // Source base of tile k (lowered by kDmaBias) and its slot.
+  auto tile_src = [&](int k) -> uint64_t {
     const int sp = k / tpp;
     if ((sp >> 6) != pte_batch) load_ptes(sp >> 6);
     const uint32_t pte = __builtin_amdgcn_readlane(pte_lane, sp & 63);
-    const uint64_t sbase = uniform_ptr(a.pool + ((uint64_t)pte << 8) + kvh * kv_head_bytes +
-                                       (uint64_t)(k % tpp) * C::T * C::KROW);
-    const uint32_t ldsb = lds_addr(dst);
-#pragma unroll
-    for (int i = 0; i < (C::NLOADS + 3) / 4; ++i) {
-      const int inst = wave + 4 * i;
-      if (inst < C::NLOADS) {
-        const int o = inst * 1024 + lane * 16;
-        uint32_t off;
-        if (C::TILE_V == 0 || o < C::TILE_K) {
-          const int row = o / C::KPITCH, w = o - row * C::KPITCH;
-          off = (uint32_t)(row * C::KROW + (w < C::KROW ? w : 0));
-        } else {
-          const int o2 = o - C::TILE_K;
-          const int row = o2 / C::VPITCH, w = o2 - row * C::VPITCH;
-          off = (uint32_t)(P * DK * 2 + row * C::VROW + (w < C::VROW ? w : 0));
-        }
-        if (C::TILE % 1024 == 0 || o < C::TILE) dma16_sbase(sbase, off, __builtin_amdgcn_readfirstlane(ldsb + inst * 1024));
-      }
+    return uniform_ptr(a.pool + ((uint64_t)pte << 8) + kvh * kv_head_bytes + (uint64_t)(k % tpp) * C::T * C::KROW -
+                       kDmaBias);
+  };
+  // Group g of this wave's loads of tile k, whose source base is sb.
+  auto issue_group = [&](int k, uint64_t sb, int g) {
+    const int n = min(4, my_loads - 4 * g);
+    if (n <= 0) return;
+    const int first = my_first + 4 * g;
+    const uint32_t lb = __builtin_amdgcn_readfirstlane(lds_addr(ring + (k % C::NBUF) * C::TILE) + first * 1024);
+    // a partial last load of the tile goes alone, with the lanes past the
+    // tile masked off
+    const bool tail = C::TILE % 1024 != 0 && first + n == C::NLOADS;
+    const int nf = tail ? n - 1 : n;
+    if (nf == 4) dma_group<4>(sb, voff[g], lb);
+    else if (nf == 3) dma_group<3>(sb, voff[g], lb);
+    else if (nf == 2) dma_group<2>(sb, voff[g], lb);
+    else if (nf == 1) dma_group<1>(sb, voff[g], lb);
+    if (tail && (C::NLOADS - 1) * 1024 + lane * 16 < C::TILE) {
+      const uint32_t last[4] = {voff[g][nf] + 1024u * nf, 0u, 0u, 0u};
+      dma_group<1>(sb, last, lb + nf * 1024);
     }
   };
-  // Loads this wave issues per tile.
-  constexpr int MY_MAX = (C::NLOADS + 3) / 4;
-  const int my_loads = (C::NLOADS - wave + 3) / 4;
+  auto issue_all = [&](int k) {
+    const uint64_t sb = tile_src(k);
+#pragma unroll
+    for (int g = 0; g < NGRP; ++g) issue_group(k, sb, g);
+  };
 
   float m[C::HBQ], lsum[C::HBQ];
   f32x4 o[C::DBW][C::HB];
@@ -164,7 +207,7 @@ __device__ __forceinline__ void wide_unit(const DecodeArgs &a, const GeomK &gm, 
   const float sl2 = gm.scale_log2;
 
   if (ntiles > 0) load_ptes(0);
-  for (int k = 0; k < C::NBUF - 1 && k < ntiles; ++k) issue(k);
+  for (int k = 0; k < C::NBUF - 1 && k < ntiles; ++k) issue_all(k);
 
 #pragma unroll 1
   for (int k = 0; k < ntiles; ++k) {
@@ -178,7 +221,12 @@ __device__ __forceinline__ void wide_unit(const DecodeArgs &a, const GeomK &gm, 
       if (later == 1) wait_vm<MY_MAX - 1>(); else if (later == 2) wait_vm<2 * (MY_MAX - 1)>(); else wait_vm<3 * (MY_MAX - 1)>();
     }
     __syncthreads();  // tile k visible to all waves; tile k-1's slot and P area are free
-    if (k + C::NBUF - 1 < ntiles) issue(k + C::NBUF - 1);
+    // loads of tile k + NBUF - 1 into the slot tile k-1 left: group 0 now,
+    // the others during the score and P.V products
+    const int kn = k + C::NBUF - 1;
+    const bool more = kn < ntiles;
+    const uint64_t sbn = more ? tile_src(kn) : 0;
+    if (more) issue_group(kn, sbn, 0);
 
     char *tb = ring + (k % C::NBUF) * C::TILE;
     const int t0 = (int)((pg_begin + (uint32_t)(k / tpp)) * P) + (k % tpp) * C::T;
@@ -222,6 +270,7 @@ __device__ __forceinline__ void wide_unit(const DecodeArgs &a, const GeomK &gm, 
             kf[(b + 1) & 1][1][j] = *reinterpret_cast<const bf16x8 *>(kr1 + 64 * ((b + 1) * KB + j));
           }
         }
+        if (NGRP > 1 && b == NKB / 2 && more) issue_group(kn, sbn, 1);
 #pragma unroll
         for (int j = 0; j < KB; ++j) {
           const int c = b * KB + j;
@@ -299,6 +348,10 @@ __device__ __forceinline__ void wide_unit(const DecodeArgs &a, const GeomK &gm, 
           }
         }
       }
+    }
+    if (more) {
+#pragma unroll
+      for (int g = 2; g < NGRP; ++g) issue_group(kn, sbn, g);
     }
     // ---- P.V for this wave's V columns, every head block
     {

@@ -15,14 +15,14 @@ enum : int32_t { kSchedBalanced = 0, kSchedQueue = 1, kSchedGrid = 2 };
 // Decode code paths (GeomK::variant), chosen per model by the host.
 //   Vector path (0-7): wavefront reductions; heads per block (16 or 8) and
 //     V values per lane (8, 4, 2, 1).
-//   Narrow matrix path (16, 17, 19, 20): 16 or 32 query heads per KV head
-//     (MLA latent head, or head_dim 128).
+//   Narrow matrix path (16, 17, 19, 20, 23): 8, 16 or 32 query heads per KV
+//     head (MLA latent head, or head_dim 128).
 //   Wide matrix path (18, 21, 22): 64 or 128 query heads per KV head; its
 //     own kernel (one workgroup per CU, scores split by heads, P.V by
 //     columns).
 enum : int32_t {
   kV16x8 = 0, kV16x4, kV16x2, kV16x1, kV8x8, kV8x4, kV8x2, kV8x1,
-  kM_MLA_G16 = 16, kM_MLA_G32, kM_MLA_G128, kM_D128_G16, kM_D128_G32, kM_D128_G64, kM_D128_G128
+  kM_MLA_G16 = 16, kM_MLA_G32, kM_MLA_G128, kM_D128_G16, kM_D128_G32, kM_D128_G64, kM_D128_G128, kM_D128_G8
 };
 constexpr bool is_wide_variant(int v) { return v == kM_MLA_G128 || v == kM_D128_G64 || v == kM_D128_G128; }
 

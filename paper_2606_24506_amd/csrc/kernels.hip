@@ -9,8 +9,8 @@
 // A page starts at pool + (pte << 8).
 #include <hip/hip_runtime.h>
 
-#include "decode_coop.h"
 #include "decode_mfma.h"
+#include "decode_narrow.h"
 #include "device_common.h"
 #include "kargs.h"
 #include "schedule.h"
@@ -255,74 +255,73 @@ __device__ __forceinline__ void valu_unit(const DecodeArgs &a, const GeomK &gm, 
   __syncthreads();  // LDS is reused by the next unit
 }
 
-template <int V> struct Mcfg;
-template <> struct Mcfg<kM_MLA_G16> { using C = CoopCfg<1, 576, 512, true, 2, 3>; };
-template <> struct Mcfg<kM_MLA_G32> { using C = CoopCfg<2, 576, 512, true, 2, 3>; };
-template <> struct Mcfg<kM_D128_G16> { using C = CoopCfg<1, 128, 128, false, 4, 3>; };
-template <> struct Mcfg<kM_D128_G32> { using C = CoopCfg<2, 128, 128, false, 4, 3>; };
+// Narrow matrix variants: heads per KV head, K and V widths, MLA layout,
+// tokens per wave slice.
+template <int V> struct NarrowVar;
+template <> struct NarrowVar<kM_MLA_G16> { static constexpr int G = 16, DK = 576, DV = 512, TW = 16; static constexpr bool MLA = true; };
+template <> struct NarrowVar<kM_MLA_G32> { static constexpr int G = 16, DK = 576, DV = 512, TW = 16; static constexpr bool MLA = true; };
+template <> struct NarrowVar<kM_D128_G8> { static constexpr int G = 8, DK = 128, DV = 128, TW = 32; static constexpr bool MLA = false; };
+template <> struct NarrowVar<kM_D128_G16> { static constexpr int G = 16, DK = 128, DV = 128, TW = 32; static constexpr bool MLA = false; };
+template <> struct NarrowVar<kM_D128_G32> { static constexpr int G = 32, DK = 128, DV = 128, TW = 32; static constexpr bool MLA = false; };
 
 template <int V>
-constexpr int mcfg_buf() { return Mcfg<V>::C::BUF; }
+constexpr int narrow_lds() {
+  using W = NarrowVar<V>;
+  return NarrowCfg<W::G, W::DK, W::DV, W::MLA, W::TW>::LDS;
+}
 
 constexpr bool has(uint32_t mask, int v) { return (mask >> v) & 1u; }
 
-// LDS bytes of one KV buffer for a kernel covering the variant set `mask`.
-constexpr int kernel_buf_bytes(uint32_t mask) {
-  int b = 0;
+// LDS bytes of a kernel covering the variant set `mask`.
+constexpr int kernel_lds_bytes(uint32_t mask) {
+  int b = 16;
   if (mask & 0xFFu) b = kLdsFloats * 4 > b ? kLdsFloats * 4 : b;
-#define CP_B(V) if (has(mask, V) && mcfg_buf<V>() > b) b = mcfg_buf<V>();
-  CP_B(kM_MLA_G16) CP_B(kM_MLA_G32) CP_B(kM_D128_G16) CP_B(kM_D128_G32)
+#define CP_B(V) if (has(mask, V) && narrow_lds<V>() > b) b = narrow_lds<V>();
+  CP_B(kM_MLA_G16) CP_B(kM_MLA_G32) CP_B(kM_D128_G8) CP_B(kM_D128_G16) CP_B(kM_D128_G32)
 #undef CP_B
   return b;
 }
 
 template <uint32_t MASK>
-__device__ __forceinline__ void run_seg(const DecodeArgs &a, const DecReq &rq, const Seg &sg, char *buf0, char *buf1,
-                                        float *red) {
+__device__ __forceinline__ void run_seg(const DecodeArgs &a, const DecReq &rq, const Seg &sg, char *lds) {
   const GeomK &gm = a.geom[rq.model];
-  float *lds = reinterpret_cast<float *>(buf0);
 #define CP_VCASE(V, HB, DPL)                                        \
   if constexpr (has(MASK, V)) {                                     \
     if (gm.variant == V) {                                          \
-      valu_unit<HB, DPL>(a, gm, rq, sg, lds);                       \
+      valu_unit<HB, DPL>(a, gm, rq, sg, reinterpret_cast<float *>(lds)); \
       return;                                                       \
     }                                                               \
   }
   CP_VCASE(kV16x8, 16, 8) CP_VCASE(kV16x4, 16, 4) CP_VCASE(kV16x2, 16, 2) CP_VCASE(kV16x1, 16, 1)
   CP_VCASE(kV8x8, 8, 8) CP_VCASE(kV8x4, 8, 4) CP_VCASE(kV8x2, 8, 2) CP_VCASE(kV8x1, 8, 1)
 #undef CP_VCASE
-#define CP_CCASE(V, HBW, DK, DV, MLA, NS, NBUF)                                      \
-  if constexpr (has(MASK, V)) {                                                      \
-    if (gm.variant == V) {                                                           \
-      coop_unit<HBW, DK, DV, MLA, NS, NBUF>(a, gm, rq, sg, buf0, buf1, red);         \
-      return;                                                                        \
-    }                                                                                \
+#define CP_NCASE(V)                                                                          \
+  if constexpr (has(MASK, V)) {                                                              \
+    if (gm.variant == V) {                                                                   \
+      using W = NarrowVar<V>;                                                                \
+      narrow_unit<W::G, W::DK, W::DV, W::MLA, W::TW>(a, gm, rq, sg, lds);                    \
+      return;                                                                                \
+    }                                                                                        \
   }
-  CP_CCASE(kM_MLA_G16, 1, 576, 512, true, 2, 3)
-  CP_CCASE(kM_MLA_G32, 2, 576, 512, true, 2, 3)
-  CP_CCASE(kM_D128_G16, 1, 128, 128, false, 4, 3)
-  CP_CCASE(kM_D128_G32, 2, 128, 128, false, 4, 3)
-#undef CP_CCASE
+  CP_NCASE(kM_MLA_G16) CP_NCASE(kM_MLA_G32) CP_NCASE(kM_D128_G8) CP_NCASE(kM_D128_G16) CP_NCASE(kM_D128_G32)
+#undef CP_NCASE
 }
 
 // One kernel per variant set of the narrow family; four waves per
-// workgroup, two KV buffers sized for the largest variant in the set.
+// workgroup, LDS sized for the largest variant in the set.
 template <uint32_t MASK>
 __global__ __launch_bounds__(256) void decode_kernel(const DecodeArgs a) {
-  constexpr int B = kernel_buf_bytes(MASK);
-  constexpr int B1 = (MASK >> 16) ? B : 16;
-  // one array, so that a ring of tiles may span both buffers
-  __shared__ __attribute__((aligned(16))) char kv[B + B1];
-  __shared__ float red[kRedFloats];
+  __shared__ __attribute__((aligned(16))) char lds[kernel_lds_bytes(MASK)];
   __shared__ uint32_t next;
-  decode_loop(a, &next, [&](const DecReq &rq, const Seg &sg) { run_seg<MASK>(a, rq, sg, kv, kv + B, red); });
+  decode_loop(a, &next, [&](const DecReq &rq, const Seg &sg) { run_seg<MASK>(a, rq, sg, lds); });
 }
 
 constexpr uint32_t vbit(int v) { return 1u << v; }
 // The variant sets the host launches together: each single variant, and
 // the mixed MLA-16 / MQA-32 / GQA-8 batch.
-constexpr uint32_t kMixedSmall = vbit(kV8x2) | vbit(kM_MLA_G16) | vbit(kM_D128_G32);
-constexpr uint32_t kAll4 = 0xFFu | vbit(kM_MLA_G16) | vbit(kM_MLA_G32) | vbit(kM_D128_G16) | vbit(kM_D128_G32);
+constexpr uint32_t kMixedSmall = vbit(kM_MLA_G16) | vbit(kM_D128_G32) | vbit(kM_D128_G8);
+constexpr uint32_t kAll4 = 0xFFu | vbit(kM_MLA_G16) | vbit(kM_MLA_G32) | vbit(kM_D128_G16) | vbit(kM_D128_G32) |
+                           vbit(kM_D128_G8);
 
 // Picks the kernel instantiation that covers `mask`. Returns
 // hipErrorInvalidValue for a set no instantiation covers (the host keeps
@@ -337,6 +336,7 @@ hipError_t launch_decode(const DecodeArgs &a, int grid, uint32_t mask, hipStream
     CP_L(vbit(kV16x8)) CP_L(vbit(kV16x4)) CP_L(vbit(kV16x2)) CP_L(vbit(kV16x1))
     CP_L(vbit(kV8x8)) CP_L(vbit(kV8x4)) CP_L(vbit(kV8x2)) CP_L(vbit(kV8x1))
     CP_L(vbit(kM_MLA_G16)) CP_L(vbit(kM_MLA_G32)) CP_L(vbit(kM_D128_G16)) CP_L(vbit(kM_D128_G32))
+    CP_L(vbit(kM_D128_G8))
     CP_L(kMixedSmall)
     default: break;
   }
@@ -350,20 +350,12 @@ hipError_t launch_decode(const DecodeArgs &a, int grid, uint32_t mask, hipStream
 
 // Workgroups of one kernel that fit on a CU at once (LDS-bound).
 int decode_wgs_per_cu(uint32_t mask) {
-  int b = 0;
-  for (int v = 0; v < 32; ++v) {
-    if (!((mask >> v) & 1u)) continue;
-    int bytes = 0;
-    switch (v) {
-      case kM_MLA_G16: bytes = 2 * mcfg_buf<kM_MLA_G16>(); break;
-      case kM_MLA_G32: bytes = 2 * mcfg_buf<kM_MLA_G32>(); break;
-      case kM_D128_G16: bytes = 2 * mcfg_buf<kM_D128_G16>(); break;
-      case kM_D128_G32: bytes = 2 * mcfg_buf<kM_D128_G32>(); break;
-      default: bytes = kLdsFloats * 4; break;
-    }
-    b = bytes > b ? bytes : b;
-  }
-  const int per = (160 * 1024) / (b + 4 * kRedFloats + 64);
+  int b = 16;
+  if (mask & 0xFFu) b = kLdsFloats * 4;
+#define CP_B(V) if (has(mask, V) && narrow_lds<V>() > b) b = narrow_lds<V>();
+  CP_B(kM_MLA_G16) CP_B(kM_MLA_G32) CP_B(kM_D128_G8) CP_B(kM_D128_G16) CP_B(kM_D128_G32)
+#undef CP_B
+  const int per = (160 * 1024) / (b + 64);
   return per < 1 ? 1 : per;
 }
 

@@ -152,7 +152,8 @@ def test_every_kernel_variant(schedule, splits):
 
 
 def test_forced_matrix_path_rejects_narrow_groups():
-    wl = custom([("gqa32x4", 10)], seed=3)
+    """One query head per KV head has no matrix-core variant."""
+    wl = custom([("gqa8x8d64", 10)], seed=3)
     ld = load(wl)
     try:
         with pytest.raises(cpl.CrossPoolError) as e:
