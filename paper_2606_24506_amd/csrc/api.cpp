@@ -20,6 +20,7 @@ hipError_t launch_gather(const GatherArgs &a, hipStream_t stream);
 hipError_t launch_decode(const DecodeArgs &a, int grid, uint32_t mask, hipStream_t stream);
 hipError_t launch_decode_wide(const DecodeArgs &a, int grid, int variant, hipStream_t stream);
 int decode_wgs_per_cu(uint32_t mask);
+int narrow_streams(int variant);
 hipError_t launch_merge(const MergeArgs &a, hipStream_t stream);
 }  // namespace cp
 
@@ -430,13 +431,13 @@ int32_t matrix_variant(const Geom &g, int32_t P) {
   return -1;
 }
 
-// Work units per KV range of a request: the narrow matrix kernel takes four
-// KV heads at once (one per wave) when the model has a multiple of four;
-// otherwise every KV head (times its head blocks on the vector path) is a
+// Work units per KV range of a request: the narrow matrix kernel takes one
+// KV head per token stream at once when the model's KV heads are a multiple
+// of its stream count; otherwise every KV head (times its head blocks) is a
 // unit of its own.
 int32_t units_per_range(const Geom &g, const GeomK &k) {
-  const bool narrow = k.variant >= kMatrixFirst && !is_wide_variant(k.variant);
-  if (narrow && g.hkv % 4 == 0) return g.hkv / 4;
+  const int ns = narrow_streams(k.variant);
+  if (ns > 0 && g.hkv % ns == 0) return g.hkv / ns;
   return g.hkv * k.nb;
 }
 
@@ -529,11 +530,11 @@ cp_status cp_attn_decode_ex(cp_pool *p, int32_t n, const int32_t *req_ids, const
   }
   if (qo > 0xFFFFFFFFull || oo > 0xFFFFFFFFull) return fail(CP_EINVAL, "batch too large");
   auto model_of = [&](int32_t i) { return p->st.req(req_ids[i]).model; };
-  // kernel family: the narrow kernel covers every vector and narrow matrix
-  // variant in one launch; each wide variant has a kernel of its own
+  // kernel family: vector variants share a launch, narrow matrix variants
+  // share another, and each wide variant has a kernel of its own
   auto wclass = [&](int32_t i) {
     const int v = gk[model_of(i)].variant;
-    return is_wide_variant(v) ? v : 0;
+    return is_wide_variant(v) ? v : (v >= kMatrixFirst ? 1 : 0);
   };
 
   // Launch groups: requests whose kernels share a workgroup size, at most

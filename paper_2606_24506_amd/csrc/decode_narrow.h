@@ -1,25 +1,29 @@
 // Matrix-core decode path for 8 to 32 query heads per KV head (MLA-16/32
-// on one latent head; MQA and GQA groups with head_dim 128). Per token and
-// KV byte there are only 8-32 flops here, so the kernel is built for memory
-// latency rather than for the matrix cores: each of the four waves of a
-// workgroup streams its own slices of TW tokens through a private two-slot
-// LDS ring, with its own online softmax, and nothing is shared between
-// waves until the unit ends. There is no barrier in the token loop, and every
-// K and V byte is read from LDS exactly once.
+// on one latent head; MQA and GQA groups with head_dim 128). Per KV byte
+// there are only 8-32 flops here, so the kernel is built to hide memory and
+// LDS latency rather than to feed the matrix cores: a workgroup of NW = 8
+// waves (two per SIMD, so one wave's stalls are the other's issue slots)
+// forms NW / SHARE token streams. A stream walks its own slices of TW
+// tokens through a private ring of NSLOT LDS slots with its own online
+// softmax; streams only meet when the unit ends. With SHARE = 2 the two
+// waves of a stream both compute the (cheap) scores of every slice and each
+// accumulates P.V for half of the V columns, which halves the accumulator
+// registers so that two waves fit a SIMD; every K byte is then read from
+// LDS twice and every V byte once.
 //
 // Per slice and 16-head block (a group of 8 heads is padded to 16):
 //   S^T[t][h] = sum_d K[t][d] Q[h][d]    mfma 16x16x32 bf16 (K rows from LDS
-//                                       as A, Q^T in registers as B; three
-//                                       independent accumulators per chain)
+//                                       as A, Q^T in registers as B; two or
+//                                       three independent accumulator chains)
 //   fp32 online softmax with a lazily moved reference maximum
 //   O^T[d][h] += sum_t V^T[d][t] P^T[t][h]
 //       TW = 16: mfma 16x16x16 bf16, B = P^T as the score lanes hold it;
 //       TW = 32: mfma 16x16x32 bf16 with the token index ordered
 //                {4q..4q+3, 16+4q..16+4q+3} for lane group q, so the two
 //                score accumulators form B as they stand.
-// Waves split a unit's work by KV head when the model has a multiple of
-// four KV heads (each wave then owns whole heads and writes them out), and
-// by token slices otherwise (slice j goes to wave j mod 4, and the four
+// Streams split a unit's work by KV head when the model's KV heads are a
+// multiple of the stream count (each stream then owns whole heads), and by
+// token slices otherwise (slice j goes to stream j mod NSTREAM, and the
 // partial softmax states are merged through LDS at the end of the unit).
 #pragma once
 
@@ -29,11 +33,10 @@ namespace cp {
 
 // G: query heads one unit handles (a model group of 8 is padded to 16; an
 // MLA group of 32 runs as two units of 16, since 32 heads x 512 columns of
-// accumulators would not leave registers for the query).
-template <int G, int DK, int DV, bool MLA, int TW>
+// accumulators would not leave registers for the rest).
+template <int G, int DK, int DV, bool MLA, int TW, int NW, int SHARE, int NSLOT>
 struct NarrowCfg {
-  static constexpr int NW = 4;
-  static constexpr int HBW = (G + 15) / 16;          // 16-head blocks per wave
+  static constexpr int HBW = (G + 15) / 16;          // 16-head blocks
   static constexpr int HEADS = 16 * HBW;             // head columns, padded
   static constexpr int KROW = DK * 2;
   static constexpr int VROW = MLA ? KROW : DV * 2;
@@ -42,66 +45,63 @@ struct NarrowCfg {
   static constexpr int SK = TW * KPITCH;
   static constexpr int SV = MLA ? 0 : TW * VPITCH;
   static constexpr int SLICE = SK + SV;              // LDS bytes of one slice
-  static constexpr int NLOADS = (SLICE + 1023) / 1024;  // 1 KiB direct loads per slice
-  static constexpr int NGRP = (NLOADS + 3) / 4;      // M0 groups per slice
-  static constexpr int NSLOT = 2;                    // ring slots per wave
-  static constexpr int RING = NW * NSLOT * SLICE;
+  static constexpr int NSTREAM = NW / SHARE;
+  static constexpr int NLOADS = (SLICE + 1023) / 1024;          // 1 KiB direct loads per slice
+  static constexpr int LOADS_M = (NLOADS + SHARE - 1) / SHARE;  // ... issued by one stream member
+  static constexpr int NGRP = (LOADS_M + 3) / 4;                // M0 groups per member and slice
+  static constexpr int RING = NSTREAM * NSLOT * SLICE;
   static constexpr int KSTEPS = DK / 32;
   static constexpr int NBLK = DV / 16;
+  static constexpr int NBLKW = NBLK / SHARE;         // V column blocks one member accumulates
   static constexpr int NSL = TW / 16;                // 16-token sub-slices
   static constexpr int NACC = KSTEPS % 3 == 0 ? 3 : 2;  // independent score chains
+  static constexpr bool AGPR_Q = HBW * KSTEPS * 4 >= 64;  // the query goes to accumulation registers
+  static constexpr int VB = NBLKW >= 8 ? 8 : NBLKW;  // V^T fragments per prefetch batch
   static constexpr int OPITCH = DV + 4;              // merge area row pitch (floats)
-  static constexpr int MERGE = HEADS * OPITCH * 4 + 2 * NW * HEADS * 4;
+  static constexpr int MERGE = HEADS * OPITCH * 4 + 2 * NSTREAM * HEADS * 4;
   static constexpr int LDS = RING > MERGE ? RING : MERGE;
   static_assert(G >= 8 && G <= 32, "8 to 32 heads per unit");
   static_assert(TW == 16 || TW == 32, "slices of 16 or 32 tokens");
-  static_assert(KSTEPS % NACC == 0, "score chains tile the k-steps");
+  static_assert(SHARE == 1 || SHARE == 2, "one or two waves per stream");
+  static_assert(NSLOT == 1 || NSLOT == 2, "one or two ring slots");
+  static_assert(SHARE == 1 || NSLOT == 2, "shared streams prefetch");
+  static_assert(KSTEPS % NACC == 0 && NBLK % SHARE == 0 && NBLKW % VB == 0, "blocking");
   static_assert(LDS <= 163840, "LDS budget");
 };
 
-template <int G, int DK, int DV, bool MLA, int TW>
+template <int G, int DK, int DV, bool MLA, int TW, int NW, int SHARE, int NSLOT>
 __device__ __forceinline__ void narrow_unit(const DecodeArgs &a, const GeomK &gm, const DecReq &rq, const Seg &sg,
                                             char *lds) {
-  using C = NarrowCfg<G, DK, DV, MLA, TW>;
+  using C = NarrowCfg<G, DK, DV, MLA, TW, NW, SHARE, NSLOT>;
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int stream = wave % C::NSTREAM, member = wave / C::NSTREAM;
   const int col = lane & 15, quad = lane >> 4;
   const int P = gm.page_tokens;  // the host routes only pages of a multiple of TW tokens here
   const int spp = P / TW;        // slices per page
   const uint32_t slot = sg.slot;
-  // work split: KV heads across waves, or token slices across waves. A
-  // group wider than one unit (gm.nb head blocks of C::HEADS) takes gm.nb
+  // Work split: KV heads across streams, or token slices across streams. A
+  // group wider than one unit (gm.nb blocks of C::HEADS heads) takes gm.nb
   // units per KV range.
-  const bool head_par = gm.hkv % 4 == 0;
+  const bool head_par = gm.hkv % C::NSTREAM == 0;
   const int nsub = gm.nb;
-  const int kvh = head_par ? 4 * (int)sg.hblk + wave : (int)sg.hblk / nsub;
+  const int kvh = head_par ? C::NSTREAM * (int)sg.hblk + stream : (int)sg.hblk / nsub;
   const int sub = head_par ? 0 : (int)sg.hblk % nsub;
   const int h0 = kvh * gm.g + sub * C::HEADS;           // first query head of the unit
   const int hv = min(C::HEADS, gm.g - sub * C::HEADS);  // valid heads (fewer when padded)
-
-  // Q^T operand fragments: lane holds head (h0 + 16 hb + col), dims
-  // 32 c + 8 quad .. +7 (zero for padded head columns).
-  bf16x8 qf[C::HBW][C::KSTEPS];
-#pragma unroll
-  for (int hb = 0; hb < C::HBW; ++hb) {
-    const int hh = 16 * hb + col;
-    const uint16_t *qrow = a.q + rq.q_off + (uint32_t)(h0 + (hh < hv ? hh : 0)) * DK + 8 * quad;
-#pragma unroll
-    for (int c = 0; c < C::KSTEPS; ++c) {
-      bf16x8 v = *reinterpret_cast<const bf16x8 *>(qrow + 32 * c);
-      if (hh >= hv) v = bf16x8{};
-      qf[hb][c] = v;
-    }
-  }
+  const int nb0 = member * C::NBLKW;                     // first V column block of this wave
 
   const uint32_t tok_begin = sg.pg_begin * (uint32_t)P;
   const uint32_t tok_end = min(rq.ctx_len, sg.pg_end * (uint32_t)P);
   const int nslices = (int)((tok_end - tok_begin + TW - 1) / TW);
-  const int first = head_par ? 0 : wave;   // this wave's first slice
-  const int step = head_par ? 1 : 4;       // ... and the stride between its slices
+  const int first = head_par ? 0 : stream;      // this stream's first slice
+  const int step = head_par ? 1 : C::NSTREAM;   // ... and the stride between its slices
   const int mine = nslices > first ? (nslices - first + step - 1) / step : 0;
+  // iterations of the loop: the same in every wave when streams share
+  // barriers (then streams with fewer slices idle through the last ones)
+  const int iters = SHARE == 1 ? mine : (head_par ? nslices : (nslices + C::NSTREAM - 1) / C::NSTREAM);
   const uint64_t kv_head_bytes = MLA ? 0 : (uint64_t)2 * P * DK * 2;
-  char *const ring = lds + wave * (C::NSLOT * C::SLICE);
+  char *const ring = lds + stream * (NSLOT * C::SLICE);
   const int npg = (int)((tok_end + P - 1) / P) - (int)sg.pg_begin;
 
   // Page-table entries of the unit, 64 at a time (lane i: page 64 b + i).
@@ -115,16 +115,18 @@ __device__ __forceinline__ void narrow_unit(const DecodeArgs &a, const GeomK &gm
     // loads: otherwise it would drain them before every use of pte_lane
     __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
   };
-  // Per-lane source offsets (biased for dma_group) of load j of a slice:
-  // load j covers LDS bytes [1024 j, 1024 j + 1024) of the slot. Pad lanes
-  // refetch the row's last 16 bytes; the lanes of a partial last load past
-  // the slice are masked off.
+  // This member's loads of a slice are [ld0, ld0 + nld); load j covers LDS
+  // bytes [1024 j, 1024 j + 1024) of the slot. Per-lane source offsets are
+  // biased for dma_group; pad lanes refetch the row's last 16 bytes; the
+  // lanes of a partial last load past the slice are masked off.
+  const int ld0 = member * C::LOADS_M;
+  const int nld = min(C::LOADS_M, C::NLOADS - ld0);
   uint32_t voff[C::NGRP][4];
 #pragma unroll
   for (int g = 0; g < C::NGRP; ++g)
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      const int o = (4 * g + j) * 1024 + lane * 16;
+      const int o = (ld0 + 4 * g + j) * 1024 + lane * 16;
       uint32_t gofs;
       if (C::SV == 0 || o < C::SK) {
         const int oc = o < C::SK ? o : 0;
@@ -137,21 +139,21 @@ __device__ __forceinline__ void narrow_unit(const DecodeArgs &a, const GeomK &gm
       }
       voff[g][j] = gofs + kDmaBias - 1024u * j;
     }
-  // Issues the loads of this wave's i-th slice into ring slot i % 2.
+  // Issues this member's loads of the stream's i-th slice into slot i % NSLOT.
   auto issue = [&](int i) {
-    const int s = first + step * i;                 // slice within the unit
-    const int sp = s / spp;                         // page within the unit
+    const int sl = first + step * i;  // slice within the unit
+    const int sp = sl / spp;          // page within the unit
     if ((sp >> 6) != pte_batch) load_ptes(sp >> 6);
     const uint32_t pte = __builtin_amdgcn_readlane(pte_lane, sp & 63);
     const uint64_t sb = uniform_ptr(a.pool + ((uint64_t)pte << 8) + (uint64_t)kvh * kv_head_bytes +
-                                    (uint64_t)(s % spp) * TW * C::KROW - kDmaBias);
-    const uint32_t lb = lds_addr(ring + (i & 1) * C::SLICE);
+                                    (uint64_t)(sl % spp) * TW * C::KROW - kDmaBias);
+    const uint32_t lb = lds_addr(ring + (i % NSLOT) * C::SLICE) + 1024 * ld0;
 #pragma unroll
     for (int g = 0; g < C::NGRP; ++g) {
-      constexpr int REM = C::NLOADS - 4 * (C::NGRP - 1);  // loads of the last group
-      const bool last = g == C::NGRP - 1;
-      const bool tail = last && C::SLICE % 1024 != 0;     // its final load is partial
-      const int nf = (last ? REM : 4) - (tail ? 1 : 0);
+      const int n = min(4, nld - 4 * g);
+      // a partial last load of the slice goes alone, lanes past it masked
+      const bool tail = C::SLICE % 1024 != 0 && ld0 + 4 * g + n == C::NLOADS;
+      const int nf = n - (tail ? 1 : 0);
       if (nf == 4) dma_group<4>(sb, voff[g], lb + 4096 * g);
       else if (nf == 3) dma_group<3>(sb, voff[g], lb + 4096 * g);
       else if (nf == 2) dma_group<2>(sb, voff[g], lb + 4096 * g);
@@ -164,41 +166,73 @@ __device__ __forceinline__ void narrow_unit(const DecodeArgs &a, const GeomK &gm
   };
 
   float m[C::HBW], lsum[C::HBW];
-  f32x4 o[C::HBW][C::NBLK];
+  f32x4 o[C::HBW][C::NBLKW];
 #pragma unroll
   for (int hb = 0; hb < C::HBW; ++hb) {
     m[hb] = -INFINITY;
     lsum[hb] = 0.f;
 #pragma unroll
-    for (int nb = 0; nb < C::NBLK; ++nb) o[hb][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int nb = 0; nb < C::NBLKW; ++nb) o[hb][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
   const float sl2 = gm.scale_log2;
   const int vrow = 4 * quad + (col >> 2);  // V row this lane supplies to a transpose read
-  const int vcol = 8 * (col & 3);
+  const int vcol = 8 * (col & 3) + 32 * nb0;
 
-  if (mine > 0) {
-    load_ptes(0);
-    issue(0);
+  // Unit start: the page-table entries, then the first slice's loads, then
+  // the query, so that the latencies of the last two overlap.
+  if (NSLOT == 2 && mine > 0) issue(0);
+  // Q^T operand fragments: lane holds head (h0 + 16 hb + col), dims
+  // 32 c + 8 quad .. +7 (zero for padded head columns).
+  bf16x8 qf[C::HBW][C::KSTEPS];
+#pragma unroll
+  for (int hb = 0; hb < C::HBW; ++hb) {
+    const int hh = 16 * hb + col;
+    const uint16_t *qrow = a.q + rq.q_off + (uint32_t)(h0 + (hh < hv ? hh : 0)) * DK + 8 * quad;
+#pragma unroll
+    for (int c = 0; c < C::KSTEPS; ++c) {
+      bf16x8 v = *reinterpret_cast<const bf16x8 *>(qrow + 32 * c);
+      if (hh >= hv) v = bf16x8{};
+      qf[hb][c] = v;
+      // a long query lives in the accumulation registers, which the matrix
+      // cores read directly as the B operand; that leaves the architectural
+      // registers to the accumulators and to fragment prefetch
+      if constexpr (C::AGPR_Q) asm volatile("" : "+a"(qf[hb][c]));
+    }
   }
+
 #pragma unroll 1
-  for (int i = 0; i < mine; ++i) {
-    if (i + 1 < mine) {
-      issue(i + 1);  // the slot of slice i-1, whose reads this wave finished
-      wait_vm<C::NLOADS>();
+  for (int i = 0; i < iters; ++i) {
+    const bool active = i < mine;
+    if constexpr (NSLOT == 1) {
+      if (active) issue(i);
+      wait_vm<0>();
+    } else if constexpr (SHARE == 1) {
+      // slice i+1 goes to the slot of slice i-1, whose reads this wave has
+      // finished, before waiting for slice i
+      if (i + 1 < mine) {
+        issue(i + 1);
+        wait_vm<C::NLOADS>();
+      } else {
+        wait_vm<0>();
+      }
     } else {
       wait_vm<0>();
+      __syncthreads();  // both members' loads of slice i landed; slot of slice i-1 free
+      if (i + 1 < mine) issue(i + 1);
     }
-    char *kt = ring + (i & 1) * C::SLICE;
+    if (!active) continue;
+    char *kt = ring + (i % NSLOT) * C::SLICE;
     char *vt = MLA ? kt : kt + C::SK;
     const int s = first + step * i;
     const int valid = min(TW, (int)(tok_end - tok_begin) - s * TW);
     if (valid < TW) {
-      // rows past the context may hold stale bytes: zero their V part so
-      // that 0 * V stays 0 (their scores are masked to -inf)
-      const int nz = (TW - valid) * (DV * 2 / 16);
-      for (int z = lane; z < nz; z += 64) {
-        const int row = valid + z / (DV * 2 / 16), pc = z % (DV * 2 / 16);
-        *reinterpret_cast<uint4 *>(vt + row * C::VPITCH + pc * 16) = make_uint4(0, 0, 0, 0);
+      // rows past the context may hold stale bytes: their scores are masked
+      // to -inf, and this wave's V columns of them are zeroed so that
+      // 0 * V stays 0 (each member zeroes only the columns it reads)
+      constexpr int CH = C::NBLKW * 2;  // 16-byte chunks of this member's columns per row
+      for (int z = lane; z < (TW - valid) * CH; z += 64) {
+        const int row = valid + z / CH, pc = z % CH;
+        *reinterpret_cast<uint4 *>(vt + row * C::VPITCH + 32 * nb0 + pc * 16) = make_uint4(0, 0, 0, 0);
       }
     }
 
@@ -212,12 +246,23 @@ __device__ __forceinline__ void narrow_unit(const DecodeArgs &a, const GeomK &gm
 #pragma unroll
         for (int hb = 0; hb < C::HBW; ++hb) acc[j][hb] = f32x4{0.f, 0.f, 0.f, 0.f};
       const char *kr = kt + (16 * u + col) * C::KPITCH + quad * 16;
+      // K fragments in batches of six, read ahead of their products (the
+      // scheduler would otherwise wait a full LDS latency per k-step)
+      constexpr int KB = C::KSTEPS % 6 == 0 ? 6 : C::KSTEPS;
 #pragma unroll
-      for (int c = 0; c < C::KSTEPS; ++c) {
-        const bf16x8 kf = *reinterpret_cast<const bf16x8 *>(kr + 64 * c);
+      for (int b = 0; b < C::KSTEPS / KB; ++b) {
+        bf16x8 kf[KB];
 #pragma unroll
-        for (int hb = 0; hb < C::HBW; ++hb)
-          acc[c % C::NACC][hb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[hb][c], acc[c % C::NACC][hb], 0, 0, 0);
+        for (int c = 0; c < KB; ++c) kf[c] = *reinterpret_cast<const bf16x8 *>(kr + 64 * (b * KB + c));
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int c = 0; c < KB; ++c)
+#pragma unroll
+          for (int hb = 0; hb < C::HBW; ++hb) {
+            const int cc = b * KB + c;
+            acc[cc % C::NACC][hb] =
+                __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[c], qf[hb][cc], acc[cc % C::NACC][hb], 0, 0, 0);
+          }
       }
 #pragma unroll
       for (int hb = 0; hb < C::HBW; ++hb) {
@@ -254,7 +299,7 @@ __device__ __forceinline__ void narrow_unit(const DecodeArgs &a, const GeomK &gm
         m[hb] = mn;
         lsum[hb] *= al;
 #pragma unroll
-        for (int nb = 0; nb < C::NBLK; ++nb) o[hb][nb] *= al;
+        for (int nb = 0; nb < C::NBLKW; ++nb) o[hb][nb] *= al;
       }
     }
     // ---- P (fp32 into the row sums, bf16 as the P.V operand) and O^T += V^T P^T
@@ -272,12 +317,29 @@ __device__ __forceinline__ void narrow_unit(const DecodeArgs &a, const GeomK &gm
         lsum[hb] += ps;
       }
       const char *vr = vt + vrow * C::VPITCH + vcol;
+      // V^T fragments in batches of VB, the next batch read while this one
+      // feeds the matrix cores
+      constexpr int NVB = C::NBLKW / C::VB;
+      s16x4 vf[2][C::VB];
 #pragma unroll
-      for (int nb = 0; nb < C::NBLK; ++nb) {
-        const s16x4 vf = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4 *)(vr + 32 * nb));
+      for (int j = 0; j < C::VB; ++j)
+        vf[0][j] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4 *)(vr + 32 * j));
 #pragma unroll
-        for (int hb = 0; hb < C::HBW; ++hb)
-          o[hb][nb] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vf, pf[hb], o[hb][nb], 0, 0, 0);
+      for (int b = 0; b < NVB; ++b) {
+        if (b + 1 < NVB) {
+#pragma unroll
+          for (int j = 0; j < C::VB; ++j)
+            vf[(b + 1) & 1][j] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                (__attribute__((address_space(3))) s16x4 *)(vr + 32 * ((b + 1) * C::VB + j)));
+        }
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int j = 0; j < C::VB; ++j)
+#pragma unroll
+          for (int hb = 0; hb < C::HBW; ++hb)
+            o[hb][b * C::VB + j] =
+                __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vf[b & 1][j], pf[hb], o[hb][b * C::VB + j], 0, 0, 0);
+        __builtin_amdgcn_sched_barrier(0);
       }
     } else {
       bf16x8 pf[C::HBW];
@@ -296,15 +358,19 @@ __device__ __forceinline__ void narrow_unit(const DecodeArgs &a, const GeomK &gm
       }
       const char *vr0 = vt + vrow * C::VPITCH + vcol;
       const char *vr1 = vr0 + 16 * C::VPITCH;
+      bf16x8 vf[C::NBLKW];
 #pragma unroll
-      for (int nb = 0; nb < C::NBLK; ++nb) {
+      for (int nb = 0; nb < C::NBLKW; ++nb) {
         const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4 *)(vr0 + 32 * nb));
         const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4 *)(vr1 + 32 * nb));
-        const bf16x8 vf = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+        vf[nb] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+      }
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int nb = 0; nb < C::NBLKW; ++nb)
 #pragma unroll
         for (int hb = 0; hb < C::HBW; ++hb)
-          o[hb][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[hb], o[hb][nb], 0, 0, 0);
-      }
+          o[hb][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf[nb], pf[hb], o[hb][nb], 0, 0, 0);
     }
   }
 
@@ -315,7 +381,7 @@ __device__ __forceinline__ void narrow_unit(const DecodeArgs &a, const GeomK &gm
     lsum[hb] += __shfl_xor(lsum[hb], 32, 64);
   }
   const bool split = rq.ws_base != kNoWs;
-  auto write_out = [&](int hh, int d, const f32x4 &v) {  // hh: head within the KV head
+  auto write_out = [&](int hh, int d, const f32x4 &v) {  // hh: head within the unit
     const uint32_t head = (uint32_t)(h0 + hh);
     if (split) {
       *reinterpret_cast<f32x4 *>(a.ws_o + ((uint64_t)rq.ws_orow + (uint64_t)slot * gm.hq + head) * DV + d) = v;
@@ -334,30 +400,34 @@ __device__ __forceinline__ void narrow_unit(const DecodeArgs &a, const GeomK &gm
       a.lse[rq.lse_off + head] = lse;
   };
   if (head_par) {
-    // this wave owns whole heads
+    // this stream owns whole heads; each member writes its V columns
 #pragma unroll
     for (int hb = 0; hb < C::HBW; ++hb) {
       const int hh = 16 * hb + col;
       if (hh < hv) {
         const float inv = 1.0f / lsum[hb];
 #pragma unroll
-        for (int nb = 0; nb < C::NBLK; ++nb) write_out(hh, 16 * nb + 4 * quad, o[hb][nb] * inv);
-        if (quad == 0) write_lse(hh, (m[hb] + fast_log2(lsum[hb])) * kLn2);
+        for (int nb = 0; nb < C::NBLKW; ++nb) write_out(hh, 16 * (nb0 + nb) + 4 * quad, o[hb][nb] * inv);
+        if (member == 0 && quad == 0) write_lse(hh, (m[hb] + fast_log2(lsum[hb])) * kLn2);
       }
     }
     __syncthreads();  // keep the waves together for the next unit
     return;
   }
-  // token slices were split over the waves: merge the four softmax states
-  float *const macc = reinterpret_cast<float *>(lds);            // [HEADS][OPITCH]
-  float *const m_x = macc + C::HEADS * C::OPITCH;                // [NW][HEADS]
-  float *const l_x = m_x + C::NW * C::HEADS;                     // [NW][HEADS]
-  __syncthreads();  // every wave is done with its ring
-  if (quad == 0) {
+  // token slices were split over the streams: merge their softmax states.
+  // Every stream writes its rescaled partial output to a region of its own
+  // (or, when those do not fit, the streams add into one region in turn).
+  constexpr bool PAR = C::NSTREAM * C::HEADS * C::OPITCH * 4 + 2 * C::NSTREAM * C::HEADS * 4 <= C::LDS;
+  constexpr int NREG = PAR ? C::NSTREAM : 1;
+  float *const macc = reinterpret_cast<float *>(lds);            // [NREG][HEADS][OPITCH]
+  float *const m_x = macc + NREG * C::HEADS * C::OPITCH;         // [NSTREAM][HEADS]
+  float *const l_x = m_x + C::NSTREAM * C::HEADS;                // [NSTREAM][HEADS]
+  __syncthreads();  // every stream is done with its ring
+  if (member == 0 && quad == 0) {
 #pragma unroll
     for (int hb = 0; hb < C::HBW; ++hb) {
-      m_x[wave * C::HEADS + 16 * hb + col] = m[hb];
-      l_x[wave * C::HEADS + 16 * hb + col] = lsum[hb];
+      m_x[stream * C::HEADS + 16 * hb + col] = m[hb];
+      l_x[stream * C::HEADS + 16 * hb + col] = lsum[hb];
     }
   }
   __syncthreads();
@@ -367,36 +437,44 @@ __device__ __forceinline__ void narrow_unit(const DecodeArgs &a, const GeomK &gm
     const int hh = 16 * hb + col;
     float M = -INFINITY;
 #pragma unroll
-    for (int w2 = 0; w2 < C::NW; ++w2) M = fmaxf(M, m_x[w2 * C::HEADS + hh]);
-    // a wave without slices has m = -inf and contributes nothing
+    for (int s2 = 0; s2 < C::NSTREAM; ++s2) M = fmaxf(M, m_x[s2 * C::HEADS + hh]);
+    // a stream without slices has m = -inf and contributes nothing
     f[hb] = m[hb] == -INFINITY ? 0.f : fast_exp2(m[hb] - M);
   }
-  for (int w2 = 0; w2 < C::NW; ++w2) {
-    if (wave == w2) {
+  auto put = [&](float *region, bool add) {
 #pragma unroll
-      for (int hb = 0; hb < C::HBW; ++hb)
+    for (int hb = 0; hb < C::HBW; ++hb)
 #pragma unroll
-        for (int nb = 0; nb < C::NBLK; ++nb) {
-          f32x4 *dst = reinterpret_cast<f32x4 *>(macc + (16 * hb + col) * C::OPITCH + 16 * nb + 4 * quad);
-          const f32x4 v = o[hb][nb] * f[hb];
-          *dst = w2 == 0 ? v : *dst + v;
-        }
-    }
+      for (int nb = 0; nb < C::NBLKW; ++nb) {
+        f32x4 *dst = reinterpret_cast<f32x4 *>(region + (16 * hb + col) * C::OPITCH + 16 * (nb0 + nb) + 4 * quad);
+        const f32x4 v = o[hb][nb] * f[hb];
+        *dst = add ? *dst + v : v;
+      }
+  };
+  if constexpr (PAR) {
+    put(macc + stream * C::HEADS * C::OPITCH, false);
     __syncthreads();
+  } else {
+    for (int s2 = 0; s2 < C::NSTREAM; ++s2) {
+      if (stream == s2) put(macc, s2 > 0);
+      __syncthreads();
+    }
   }
   // normalise and write: four consecutive values per thread
-  for (int e = threadIdx.x; e < hv * DV / 4; e += 256) {
+  for (int e = threadIdx.x; e < hv * DV / 4; e += 64 * NW) {
     const int hh = (4 * e) / DV, d = (4 * e) % DV;
     float M = -INFINITY, L = 0.f;
 #pragma unroll
-    for (int w2 = 0; w2 < C::NW; ++w2) M = fmaxf(M, m_x[w2 * C::HEADS + hh]);
+    for (int s2 = 0; s2 < C::NSTREAM; ++s2) M = fmaxf(M, m_x[s2 * C::HEADS + hh]);
 #pragma unroll
-    for (int w2 = 0; w2 < C::NW; ++w2) {
-      const float mw = m_x[w2 * C::HEADS + hh];
-      L += mw == -INFINITY ? 0.f : l_x[w2 * C::HEADS + hh] * fast_exp2(mw - M);
+    for (int s2 = 0; s2 < C::NSTREAM; ++s2) {
+      const float ms = m_x[s2 * C::HEADS + hh];
+      L += ms == -INFINITY ? 0.f : l_x[s2 * C::HEADS + hh] * fast_exp2(ms - M);
     }
-    const f32x4 v = *reinterpret_cast<const f32x4 *>(macc + hh * C::OPITCH + d) * (1.0f / L);
-    write_out(hh, d, v);
+    f32x4 v = *reinterpret_cast<const f32x4 *>(macc + hh * C::OPITCH + d);
+#pragma unroll
+    for (int r = 1; r < NREG; ++r) v += *reinterpret_cast<const f32x4 *>(macc + (r * C::HEADS + hh) * C::OPITCH + d);
+    write_out(hh, d, v * (1.0f / L));
     if (d == 0) write_lse(hh, (M + fast_log2(L)) * kLn2);
   }
   __syncthreads();  // LDS is reused by the next unit

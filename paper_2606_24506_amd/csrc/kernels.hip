@@ -255,27 +255,30 @@ __device__ __forceinline__ void valu_unit(const DecodeArgs &a, const GeomK &gm, 
   __syncthreads();  // LDS is reused by the next unit
 }
 
-// Narrow matrix variants: heads per KV head, K and V widths, MLA layout,
-// tokens per wave slice.
+// Narrow matrix variants: heads per unit, K and V widths, MLA layout,
+// tokens per slice, and the stream layout of the 8-wave workgroup (waves
+// per stream, ring slots per stream).
+constexpr int kNarrowWaves = 8;
 template <int V> struct NarrowVar;
-template <> struct NarrowVar<kM_MLA_G16> { static constexpr int G = 16, DK = 576, DV = 512, TW = 16; static constexpr bool MLA = true; };
-template <> struct NarrowVar<kM_MLA_G32> { static constexpr int G = 16, DK = 576, DV = 512, TW = 16; static constexpr bool MLA = true; };
-template <> struct NarrowVar<kM_D128_G8> { static constexpr int G = 8, DK = 128, DV = 128, TW = 32; static constexpr bool MLA = false; };
-template <> struct NarrowVar<kM_D128_G16> { static constexpr int G = 16, DK = 128, DV = 128, TW = 32; static constexpr bool MLA = false; };
-template <> struct NarrowVar<kM_D128_G32> { static constexpr int G = 32, DK = 128, DV = 128, TW = 32; static constexpr bool MLA = false; };
+template <> struct NarrowVar<kM_MLA_G16> { static constexpr int G = 16, DK = 576, DV = 512, TW = 16, SHARE = 2, NSLOT = 2; static constexpr bool MLA = true; };
+template <> struct NarrowVar<kM_MLA_G32> { static constexpr int G = 16, DK = 576, DV = 512, TW = 16, SHARE = 2, NSLOT = 2; static constexpr bool MLA = true; };
+template <> struct NarrowVar<kM_D128_G8> { static constexpr int G = 8, DK = 128, DV = 128, TW = 32, SHARE = 2, NSLOT = 2; static constexpr bool MLA = false; };
+template <> struct NarrowVar<kM_D128_G16> { static constexpr int G = 16, DK = 128, DV = 128, TW = 32, SHARE = 2, NSLOT = 2; static constexpr bool MLA = false; };
+template <> struct NarrowVar<kM_D128_G32> { static constexpr int G = 32, DK = 128, DV = 128, TW = 32, SHARE = 2, NSLOT = 2; static constexpr bool MLA = false; };
+template <int V>
+using NarrowCfgOf = NarrowCfg<NarrowVar<V>::G, NarrowVar<V>::DK, NarrowVar<V>::DV, NarrowVar<V>::MLA, NarrowVar<V>::TW,
+                              kNarrowWaves, NarrowVar<V>::SHARE, NarrowVar<V>::NSLOT>;
 
 template <int V>
-constexpr int narrow_lds() {
-  using W = NarrowVar<V>;
-  return NarrowCfg<W::G, W::DK, W::DV, W::MLA, W::TW>::LDS;
-}
+constexpr int narrow_lds() { return NarrowCfgOf<V>::LDS; }
 
 constexpr bool has(uint32_t mask, int v) { return (mask >> v) & 1u; }
+constexpr uint32_t kValuMask = 0xFFu;
 
 // LDS bytes of a kernel covering the variant set `mask`.
 constexpr int kernel_lds_bytes(uint32_t mask) {
   int b = 16;
-  if (mask & 0xFFu) b = kLdsFloats * 4 > b ? kLdsFloats * 4 : b;
+  if (mask & kValuMask) b = kLdsFloats * 4 > b ? kLdsFloats * 4 : b;
 #define CP_B(V) if (has(mask, V) && narrow_lds<V>() > b) b = narrow_lds<V>();
   CP_B(kM_MLA_G16) CP_B(kM_MLA_G32) CP_B(kM_D128_G8) CP_B(kM_D128_G16) CP_B(kM_D128_G32)
 #undef CP_B
@@ -299,7 +302,7 @@ __device__ __forceinline__ void run_seg(const DecodeArgs &a, const DecReq &rq, c
   if constexpr (has(MASK, V)) {                                                              \
     if (gm.variant == V) {                                                                   \
       using W = NarrowVar<V>;                                                                \
-      narrow_unit<W::G, W::DK, W::DV, W::MLA, W::TW>(a, gm, rq, sg, lds);                    \
+      narrow_unit<W::G, W::DK, W::DV, W::MLA, W::TW, kNarrowWaves, W::SHARE, W::NSLOT>(a, gm, rq, sg, lds); \
       return;                                                                                \
     }                                                                                        \
   }
@@ -309,8 +312,14 @@ __device__ __forceinline__ void run_seg(const DecodeArgs &a, const DecReq &rq, c
 
 // One kernel per variant set of the narrow family; four waves per
 // workgroup, LDS sized for the largest variant in the set.
+// Vector variants run four waves per workgroup, narrow matrix variants
+// eight; the host never mixes the two families in one launch.
 template <uint32_t MASK>
-__global__ __launch_bounds__(256) void decode_kernel(const DecodeArgs a) {
+constexpr int kernel_waves() { return (MASK & kValuMask) ? 4 : kNarrowWaves; }
+
+template <uint32_t MASK>
+__global__ __launch_bounds__(64 * kernel_waves<MASK>()) void decode_kernel(const DecodeArgs a) {
+  static_assert(!((MASK & kValuMask) && (MASK & ~kValuMask)), "vector and matrix variants launch separately");
   __shared__ __attribute__((aligned(16))) char lds[kernel_lds_bytes(MASK)];
   __shared__ uint32_t next;
   decode_loop(a, &next, [&](const DecReq &rq, const Seg &sg) { run_seg<MASK>(a, rq, sg, lds); });
@@ -320,8 +329,8 @@ constexpr uint32_t vbit(int v) { return 1u << v; }
 // The variant sets the host launches together: each single variant, and
 // the mixed MLA-16 / MQA-32 / GQA-8 batch.
 constexpr uint32_t kMixedSmall = vbit(kM_MLA_G16) | vbit(kM_D128_G32) | vbit(kM_D128_G8);
-constexpr uint32_t kAll4 = 0xFFu | vbit(kM_MLA_G16) | vbit(kM_MLA_G32) | vbit(kM_D128_G16) | vbit(kM_D128_G32) |
-                           vbit(kM_D128_G8);
+constexpr uint32_t kAllNarrow =
+    vbit(kM_MLA_G16) | vbit(kM_MLA_G32) | vbit(kM_D128_G16) | vbit(kM_D128_G32) | vbit(kM_D128_G8);
 
 // Picks the kernel instantiation that covers `mask`. Returns
 // hipErrorInvalidValue for a set no instantiation covers (the host keeps
@@ -330,7 +339,7 @@ hipError_t launch_decode(const DecodeArgs &a, int grid, uint32_t mask, hipStream
   const dim3 g(grid);
 #define CP_L(M)                                                                       \
   case M:                                                                             \
-    hipLaunchKernelGGL((decode_kernel<M>), g, dim3(256), 0, stream, a);               \
+    hipLaunchKernelGGL((decode_kernel<M>), g, dim3(64 * kernel_waves<M>()), 0, stream, a); \
     return hipGetLastError();
   switch (mask) {
     CP_L(vbit(kV16x8)) CP_L(vbit(kV16x4)) CP_L(vbit(kV16x2)) CP_L(vbit(kV16x1))
@@ -341,11 +350,28 @@ hipError_t launch_decode(const DecodeArgs &a, int grid, uint32_t mask, hipStream
     default: break;
   }
 #undef CP_L
-  if ((mask & ~kAll4) == 0) {
-    hipLaunchKernelGGL((decode_kernel<kAll4>), g, dim3(256), 0, stream, a);
+  if ((mask & ~kValuMask) == 0) {
+    hipLaunchKernelGGL((decode_kernel<kValuMask>), g, dim3(256), 0, stream, a);
+    return hipGetLastError();
+  }
+  if ((mask & ~kAllNarrow) == 0) {
+    hipLaunchKernelGGL((decode_kernel<kAllNarrow>), g, dim3(64 * kNarrowWaves), 0, stream, a);
     return hipGetLastError();
   }
   return hipErrorInvalidValue;
+}
+
+// Token streams of the narrow kernel for a variant (KV heads a unit covers
+// when they split across streams).
+int narrow_streams(int variant) {
+  switch (variant) {
+    case kM_MLA_G16: return NarrowCfgOf<kM_MLA_G16>::NSTREAM;
+    case kM_MLA_G32: return NarrowCfgOf<kM_MLA_G32>::NSTREAM;
+    case kM_D128_G8: return NarrowCfgOf<kM_D128_G8>::NSTREAM;
+    case kM_D128_G16: return NarrowCfgOf<kM_D128_G16>::NSTREAM;
+    case kM_D128_G32: return NarrowCfgOf<kM_D128_G32>::NSTREAM;
+    default: return 0;
+  }
 }
 
 // Workgroups of one kernel that fit on a CU at once (LDS-bound).
