@@ -80,4 +80,30 @@ CP_DEV void wait_vm() {
 
 CP_DEV uint32_t lds_addr(const void *p) { return (uint32_t)(uintptr_t)p; }
 
+// Row pitch of K and V tiles in LDS: a row of R bytes (a multiple of 128)
+// plus 32 bytes. With rows 2 mod 8 16-byte chunks apart, both the K operand
+// reads (16 rows x 16 bytes per lane group) and the V transpose reads of
+// these kernels are free of bank conflicts on gfx950; a 16-byte pad (1 mod
+// 8) halves their rate, an unpadded row quarters it.
+constexpr int lds_pitch(int row_bytes) { return row_bytes + 32; }
+
+// Reductions over lanes l, l^16, l^32, l^48 (the four lane groups that hold
+// one column of an mfma 16x16 result), by the gfx950 half-row and half-wave
+// swaps: a swap of x with itself leaves lane l's partner value in one of the
+// two results and its own in the other, so the pair reduces to both.
+CP_DEV float xor_max_16_32(float x) {
+  auto p = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  const float a = __uint_as_float(p[0]), b = __uint_as_float(p[1]);
+  const float y = a > b ? a : b;
+  auto q = __builtin_amdgcn_permlane16_swap(__float_as_uint(y), __float_as_uint(y), false, false);
+  const float c = __uint_as_float(q[0]), d = __uint_as_float(q[1]);
+  return c > d ? c : d;
+}
+CP_DEV float xor_sum_16_32(float x) {
+  auto p = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  const float y = __uint_as_float(p[0]) + __uint_as_float(p[1]);
+  auto q = __builtin_amdgcn_permlane16_swap(__float_as_uint(y), __float_as_uint(y), false, false);
+  return __uint_as_float(q[0]) + __uint_as_float(q[1]);
+}
+
 }  // namespace cp

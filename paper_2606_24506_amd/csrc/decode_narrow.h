@@ -40,8 +40,8 @@ struct NarrowCfg {
   static constexpr int HEADS = 16 * HBW;             // head columns, padded
   static constexpr int KROW = DK * 2;
   static constexpr int VROW = MLA ? KROW : DV * 2;
-  static constexpr int KPITCH = KROW + 16;           // 16-byte pad spreads LDS banks
-  static constexpr int VPITCH = MLA ? KPITCH : VROW + 16;
+  static constexpr int KPITCH = lds_pitch(KROW);     // padded rows: conflict-free LDS reads
+  static constexpr int VPITCH = MLA ? KPITCH : lds_pitch(VROW);
   static constexpr int SK = TW * KPITCH;
   static constexpr int SV = MLA ? 0 : TW * VPITCH;
   static constexpr int SLICE = SK + SV;              // LDS bytes of one slice
@@ -286,8 +286,7 @@ __device__ __forceinline__ void narrow_unit(const DecodeArgs &a, const GeomK &gm
           sv[u][hb][r] = v;
           x = fmaxf(x, v);
         }
-      x = fmaxf(x, __shfl_xor(x, 16, 64));
-      x = fmaxf(x, __shfl_xor(x, 32, 64));
+      x = xor_max_16_32(x);
       mt[hb] = x;
       bump = bump || x > m[hb] + kLazy;
     }
@@ -377,8 +376,7 @@ __device__ __forceinline__ void narrow_unit(const DecodeArgs &a, const GeomK &gm
   // ---- unit end
 #pragma unroll
   for (int hb = 0; hb < C::HBW; ++hb) {
-    lsum[hb] += __shfl_xor(lsum[hb], 16, 64);
-    lsum[hb] += __shfl_xor(lsum[hb], 32, 64);
+    lsum[hb] = xor_sum_16_32(lsum[hb]);
   }
   const bool split = rq.ws_base != kNoWs;
   auto write_out = [&](int hh, int d, const f32x4 &v) {  // hh: head within the unit

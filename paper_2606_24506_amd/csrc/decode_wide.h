@@ -41,8 +41,8 @@ struct WideCfg {
   static constexpr int NW = 4, T = 32;
   static constexpr int KROW = DK * 2;                // bytes of one K row in HBM
   static constexpr int VROW = MLA ? KROW : DV * 2;   // ... of one V row
-  static constexpr int KPITCH = KROW + 16;           // LDS row pitches (16-byte pad spreads banks)
-  static constexpr int VPITCH = MLA ? KPITCH : VROW + 16;
+  static constexpr int KPITCH = lds_pitch(KROW);     // padded LDS rows: conflict-free reads
+  static constexpr int VPITCH = MLA ? KPITCH : lds_pitch(VROW);
   static constexpr int TILE_K = T * KPITCH;
   static constexpr int TILE_V = MLA ? 0 : T * VPITCH;
   static constexpr int TILE = TILE_K + TILE_V;       // LDS bytes of one tile
@@ -134,8 +134,8 @@ __device__ __forceinline__ void wide_unit(const DecodeArgs &a, const GeomK &gm, 
   // contiguous range of loads, in groups of up to four per M0 write
   // (dma_group); the groups are spread over the tile's work so that an M0
   // write rarely finds the previous group still queued. Lanes on a row's
-  // 16-byte pad fetch the row's last 16 bytes again (same cache line, never
-  // read back); lanes past the tile are masked off.
+  // pad fetch the row's last 16 bytes again (same cache line, never read
+  // back); lanes past the tile are masked off.
   constexpr int LBASE = C::NLOADS / 4, LREM = C::NLOADS % 4;
   constexpr int MY_MAX = LBASE + (LREM ? 1 : 0);  // loads of the busiest wave
   constexpr int NGRP = (MY_MAX + 3) / 4;          // M0 groups per wave and tile
@@ -300,8 +300,7 @@ __device__ __forceinline__ void wide_unit(const DecodeArgs &a, const GeomK &gm, 
           s[sl][hb][r] = v;
           x = fmaxf(x, v);
         }
-      x = fmaxf(x, __shfl_xor(x, 16, 64));
-      x = fmaxf(x, __shfl_xor(x, 32, 64));
+      x = xor_max_16_32(x);
       mt[hb] = x;
       bump = bump || x > m[hb] + kLazy;
     }
@@ -387,8 +386,7 @@ __device__ __forceinline__ void wide_unit(const DecodeArgs &a, const GeomK &gm, 
   // ---- final: score waves publish m and l; every wave normalises its columns
 #pragma unroll
   for (int hb = 0; hb < C::HBQ; ++hb) {
-    lsum[hb] += __shfl_xor(lsum[hb], 16, 64);
-    lsum[hb] += __shfl_xor(lsum[hb], 32, 64);
+    lsum[hb] = xor_sum_16_32(lsum[hb]);
   }
   __syncthreads();  // last tile's P area is no longer read
   if (quad == 0) {
