@@ -273,20 +273,27 @@ __device__ __forceinline__ void narrow_unit(const DecodeArgs &a, const GeomK &gm
       }
     }
     // ---- online softmax (lane owns head column col; rows 16 u + 4 quad + r)
+    // (scores stay unscaled: the positive scale goes onto the column maximum
+    // and into the exponent's fma)
+    if (valid < TW) {
+#pragma unroll
+      for (int u = 0; u < C::NSL; ++u)
+#pragma unroll
+        for (int hb = 0; hb < C::HBW; ++hb)
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            if (16 * u + 4 * quad + r >= valid) sv[u][hb][r] = -INFINITY;
+    }
     bool bump = false;
     float mt[C::HBW];
 #pragma unroll
     for (int hb = 0; hb < C::HBW; ++hb) {
-      float x = -INFINITY;
+      float x = sv[0][hb][0];
 #pragma unroll
       for (int u = 0; u < C::NSL; ++u)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const float v = 16 * u + 4 * quad + r < valid ? sv[u][hb][r] * sl2 : -INFINITY;
-          sv[u][hb][r] = v;
-          x = fmaxf(x, v);
-        }
-      x = xor_max_16_32(x);
+        for (int r = 0; r < 4; ++r) x = x > sv[u][hb][r] ? x : sv[u][hb][r];
+      x = xor_max_16_32(x) * sl2;
       mt[hb] = x;
       bump = bump || x > m[hb] + kLazy;
     }
@@ -309,7 +316,7 @@ __device__ __forceinline__ void narrow_unit(const DecodeArgs &a, const GeomK &gm
         float ps = 0.f;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const float p = fast_exp2(sv[0][hb][r] - m[hb]);
+          const float p = fast_exp2(__builtin_fmaf(sv[0][hb][r], sl2, -m[hb]));
           ps += p;
           pf[hb][r] = __builtin_bit_cast(short, (__bf16)p);
         }
@@ -349,7 +356,7 @@ __device__ __forceinline__ void narrow_unit(const DecodeArgs &a, const GeomK &gm
         for (int u = 0; u < 2; ++u)
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
-            const float p = fast_exp2(sv[u][hb][r] - m[hb]);
+            const float p = fast_exp2(__builtin_fmaf(sv[u][hb][r], sl2, -m[hb]));
             ps += p;
             pf[hb][4 * u + r] = (__bf16)p;
           }

@@ -286,21 +286,28 @@ __device__ __forceinline__ void wide_unit(const DecodeArgs &a, const GeomK &gm, 
         }
       }
     }
-    // ---- online softmax per head (lane owns head column col; rows 4 quad + r)
+    // ---- online softmax per head (lane owns head column col; rows 4 quad + r).
+    // Scores stay unscaled: the scale (positive) is applied to the column
+    // maximum and folded into the exponent's fma.
+    if (valid < C::T) {
+#pragma unroll
+      for (int sl = 0; sl < 2; ++sl)
+#pragma unroll
+        for (int hb = 0; hb < C::HBQ; ++hb)
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            if (16 * sl + 4 * quad + r >= valid) s[sl][hb][r] = -INFINITY;
+    }
     bool bump = false;
     float mt[C::HBQ];
 #pragma unroll
     for (int hb = 0; hb < C::HBQ; ++hb) {
-      float x = -INFINITY;
+      float x = s[0][hb][0];
 #pragma unroll
       for (int sl = 0; sl < 2; ++sl)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const float v = 16 * sl + 4 * quad + r < valid ? s[sl][hb][r] * sl2 : -INFINITY;
-          s[sl][hb][r] = v;
-          x = fmaxf(x, v);
-        }
-      x = xor_max_16_32(x);
+        for (int r = 0; r < 4; ++r) x = x > s[sl][hb][r] ? x : s[sl][hb][r];
+      x = xor_max_16_32(x) * sl2;
       mt[hb] = x;
       bump = bump || x > m[hb] + kLazy;
     }
@@ -325,7 +332,7 @@ __device__ __forceinline__ void wide_unit(const DecodeArgs &a, const GeomK &gm, 
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           // the row sum takes p in fp32; only the P.V operand is rounded to bf16
-          const float p = fast_exp2(s[sl][hb][r] - m[hb]);
+          const float p = fast_exp2(__builtin_fmaf(s[sl][hb][r], sl2, -m[hb]));
           ps += p;
           pk[4 * sl + r] = (__bf16)p;
         }

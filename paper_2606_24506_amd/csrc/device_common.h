@@ -37,6 +37,18 @@ CP_DEV float wave_sum(float v) {
   return v;
 }
 
+// Index of the last of n (<= 64) non-decreasing keys key(0..n-1) that is
+// <= x, or 0 when none is. The lanes test one key each and a ballot counts
+// the passing prefix, so the search costs one load latency instead of a
+// chain of dependent scalar loads from the argument segment. key(0) is not
+// read; every lane of the wave must take part.
+template <class F>
+CP_DEV int sorted_search(int n, uint64_t x, F key) {
+  const int lane = threadIdx.x & 63;
+  const bool le = lane > 0 && lane < n && (uint64_t)key(lane) <= x;
+  return __builtin_popcountll(__builtin_amdgcn_ballot_w64(le));
+}
+
 CP_DEV const uint8_t *page_ptr(const uint8_t *pool, const uint32_t *pte, uint32_t pte_base, uint32_t page) {
   return pool + ((uint64_t)pte[pte_base + page] << 8);
 }

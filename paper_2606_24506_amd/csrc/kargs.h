@@ -8,7 +8,7 @@
 namespace cp {
 
 constexpr int kMaxLaunchModels = 4;   // distinct models in one decode launch
-constexpr int kMaxReqPerLaunch = 64;  // requests in one launch
+constexpr int kMaxReqPerLaunch = 64;  // requests in one launch (at most one per lane of a wave)
 constexpr uint32_t kNoWs = 0xFFFFFFFFu;
 enum : int32_t { kSchedBalanced = 0, kSchedQueue = 1, kSchedGrid = 2 };
 
@@ -119,6 +119,7 @@ struct GatherArgs {
   GeomK geom;
 };
 
+static_assert(kMaxReqPerLaunch <= 64, "request lookups search one key per lane");
 static_assert(sizeof(DecodeArgs) <= 3072, "decode kernel arguments too large");
 static_assert(sizeof(MergeArgs) <= 3072, "merge kernel arguments too large");
 static_assert(sizeof(AppendArgs) <= 3072, "append kernel arguments too large");

@@ -22,8 +22,7 @@ namespace cp {
 // One workgroup per appended row; threads copy 16-byte segments.
 __global__ __launch_bounds__(256) void kv_append_kernel(const AppendArgs a) {
   const uint32_t row = blockIdx.x;
-  int r = 0;
-  while (r + 1 < a.n_req && a.req[r + 1].row_begin <= row) ++r;
+  const int r = sorted_search(a.n_req, row, [&](int i) { return a.req[i].row_begin; });
   const AppReq &rq = a.req[r];
   const GeomK &g = a.geom[rq.model];
   const uint32_t pos = rq.old_len + (row - rq.row_begin);
@@ -397,8 +396,7 @@ __global__ __launch_bounds__(256) void merge_kernel(const MergeArgs a) {
   __shared__ float red[4];
   __shared__ float part[3][128];
   const uint32_t nblk_total = blockIdx.x;
-  int r = 0;
-  while (r + 1 < a.n_req && a.req[r + 1].block_begin <= nblk_total) ++r;
+  const int r = sorted_search(a.n_req, nblk_total, [&](int i) { return a.req[i].block_begin; });
   const MergeReq &rq = a.req[r];
   const uint32_t dblocks = rq.d_v / 128 ? rq.d_v / 128 : 1;
   const uint32_t local = nblk_total - rq.block_begin;

@@ -7,6 +7,7 @@
 
 #include <hip/hip_runtime.h>
 
+#include "device_common.h"
 #include "kargs.h"
 
 namespace cp {
@@ -38,8 +39,7 @@ __device__ __forceinline__ bool next_balanced(const DecodeArgs &a, int *r, uint3
 
 // Decodes unit u of the queue and grid schedules into (request, piece).
 __device__ __forceinline__ int unit_segment(const DecodeArgs &a, uint32_t u, Seg *sg) {
-  int r = 0;
-  while (r + 1 < a.n_req && a.req[r + 1].unit_begin <= u) ++r;
+  const int r = sorted_search(a.n_req, u, [&](int i) { return a.req[i].unit_begin; });
   const DecReq &rq = a.req[r];
   const uint32_t local = u - rq.unit_begin;
   const uint32_t chunk = local / rq.n_hblk;
@@ -57,7 +57,12 @@ __device__ __forceinline__ int unit_segment(const DecodeArgs &a, uint32_t u, Seg
 // launch.
 template <class F>
 __device__ __forceinline__ void decode_loop(const DecodeArgs &a, uint32_t *next, F &&seg) {
-  int br = 0;        // balanced: request being searched
+  // balanced: request being searched, starting with the one that holds the
+  // first cost unit of this workgroup's share
+  int br = a.schedule == kSchedBalanced
+               ? sorted_search(a.n_req, (uint64_t)blockIdx.x * a.total_cost / gridDim.x,
+                               [&](int i) { return a.req[i].unit_begin; })
+               : 0;
   uint32_t bhb = 0;  // balanced: next head block of that request
   bool first = true;
   for (;;) {
