@@ -57,7 +57,7 @@ struct NarrowCfg {
   static constexpr int NACC = KSTEPS % 3 == 0 ? 3 : 2;  // independent score chains
   static constexpr bool AGPR_Q = HBW * KSTEPS * 4 >= 64;  // the query goes to accumulation registers
   static constexpr int VB = NBLKW >= 8 ? 8 : NBLKW;  // V^T fragments per prefetch batch
-  static constexpr int OPITCH = DV + 4;              // merge area row pitch (floats)
+  static constexpr int OPITCH = DV + 8;              // merge area row pitch (floats; 2 mod 8 16-byte chunks)
   static constexpr int MERGE = HEADS * OPITCH * 4 + 2 * NSTREAM * HEADS * 4;
   static constexpr int LDS = RING > MERGE ? RING : MERGE;
   static_assert(G >= 8 && G <= 32, "8 to 32 heads per unit");
@@ -465,9 +465,14 @@ __device__ __forceinline__ void narrow_unit(const DecodeArgs &a, const GeomK &gm
       __syncthreads();
     }
   }
-  // normalise and write: four consecutive values per thread
-  for (int e = threadIdx.x; e < hv * DV / 4; e += 64 * NW) {
-    const int hh = (4 * e) / DV, d = (4 * e) % DV;
+  // normalise and write: thread t takes head t / TPH and the 16-byte column
+  // chunks t % TPH + TPH j (conflict-free LDS reads, coalesced stores); the
+  // head's merged m and l are formed once
+  {
+    constexpr int TPH = 64 * NW / C::HEADS;  // threads per head
+    constexpr int NCH = DV / 4 / TPH;        // 16-byte chunks per thread
+    static_assert(NCH >= 1 && (DV / 4) % TPH == 0, "whole chunks per thread");
+    const int hh = threadIdx.x / TPH, ci = threadIdx.x % TPH;
     float M = -INFINITY, L = 0.f;
 #pragma unroll
     for (int s2 = 0; s2 < C::NSTREAM; ++s2) M = fmaxf(M, m_x[s2 * C::HEADS + hh]);
@@ -476,11 +481,16 @@ __device__ __forceinline__ void narrow_unit(const DecodeArgs &a, const GeomK &gm
       const float ms = m_x[s2 * C::HEADS + hh];
       L += ms == -INFINITY ? 0.f : l_x[s2 * C::HEADS + hh] * fast_exp2(ms - M);
     }
-    f32x4 v = *reinterpret_cast<const f32x4 *>(macc + hh * C::OPITCH + d);
+    const float inv = 1.0f / L;
+#pragma unroll 1
+    for (int j = 0; j < NCH; ++j) {
+      const int d = 4 * (ci + TPH * j);
+      f32x4 v = *reinterpret_cast<const f32x4 *>(macc + hh * C::OPITCH + d);
 #pragma unroll
-    for (int r = 1; r < NREG; ++r) v += *reinterpret_cast<const f32x4 *>(macc + (r * C::HEADS + hh) * C::OPITCH + d);
-    write_out(hh, d, v * (1.0f / L));
-    if (d == 0) write_lse(hh, (M + fast_log2(L)) * kLn2);
+      for (int r = 1; r < NREG; ++r) v += *reinterpret_cast<const f32x4 *>(macc + (r * C::HEADS + hh) * C::OPITCH + d);
+      if (hh < hv) write_out(hh, d, v * inv);
+    }
+    if (hh < hv && ci == 0) write_lse(hh, (M + fast_log2(L)) * kLn2);
   }
   __syncthreads();  // LDS is reused by the next unit
 }
