@@ -583,7 +583,7 @@ cp_status cp_attn_decode_ex(cp_pool *p, int32_t n, const int32_t *req_ids, const
       for (int32_t i : g.idx) {
         const uint64_t c = (uint64_t)gk[model_of(i)].page_cost;
         cost_prefix[i] = (uint32_t)T;
-        T += (uint64_t)pages[i] * c;
+        T += (kPieceFixedPages + (uint64_t)pages[i]) * c;
         maxc = std::max(maxc, c);
       }
       if (T > 0xFFFFFFFFull) return fail(CP_EINVAL, "batch too large for one launch");
@@ -592,7 +592,8 @@ cp_status cp_attn_decode_ex(cp_pool *p, int32_t n, const int32_t *req_ids, const
       const uint64_t W = std::max<uint64_t>(1, std::min<uint64_t>((uint64_t)slots, T / maxc));
       auto owner = [&](uint64_t x) { return (uint32_t)(((x + 1) * W - 1) / T); };
       for (int32_t i : g.idx) {
-        const uint64_t c = (uint64_t)gk[model_of(i)].page_cost, C = cost_prefix[i];
+        // page j of the request sits at C + j c, after the fixed cost
+        const uint64_t c = (uint64_t)gk[model_of(i)].page_cost, C = cost_prefix[i] + kPieceFixedPages * c;
         const uint32_t w0 = owner(C), w1 = owner(C + (uint64_t)(pages[i] - 1) * c);
         first_worker[i] = (int32_t)w0;
         n_slots[i] = (int32_t)(w1 - w0 + 1);
