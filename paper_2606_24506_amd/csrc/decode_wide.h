@@ -33,12 +33,12 @@ namespace cp {
 
 typedef unsigned int u32x4v __attribute__((ext_vector_type(4)));
 
-// QL: the last QL of the KSTEPS query k-steps are kept in LDS rather than
-// registers (MLA-128 needs 256 accumulator registers for P.V plus 144 for
-// the whole query, which leaves too little for the pipelines).
-template <int G, int DK, int DV, bool MLA, int QL = 0>
+// NW: waves of the workgroup (4 or 8; with 8, two waves share each SIMD,
+// so one's LDS and softmax latencies are the other's issue slots). QL: the
+// last QL of the KSTEPS query k-steps are kept in LDS rather than registers.
+template <int G, int DK, int DV, bool MLA, int QL, int NW_>
 struct WideCfg {
-  static constexpr int NW = 4, T = 32;
+  static constexpr int NW = NW_, T = 32;
   static constexpr int KROW = DK * 2;                // bytes of one K row in HBM
   static constexpr int VROW = MLA ? KROW : DV * 2;   // ... of one V row
   static constexpr int KPITCH = lds_pitch(KROW);     // padded LDS rows: conflict-free reads
@@ -49,29 +49,34 @@ struct WideCfg {
   static constexpr int NLOADS = (TILE + 1023) / 1024;  // 1 KiB direct loads per tile
   static constexpr int KSTEPS = DK / 32;
   static constexpr int HB = G / 16;                  // head blocks of the KV head
-  static constexpr int HBQ = G / 64;                 // head blocks each wave scores
-  static constexpr int DBW = DV / 64;                // V column blocks each wave accumulates
+  static constexpr int HBQ = G / (16 * NW);          // head blocks each wave scores
+  static constexpr int DBW = DV / (16 * NW);         // V column blocks each wave accumulates
   static constexpr int QR = KSTEPS - QL;             // query k-steps held in registers
-  static constexpr bool AGPR_Q = HB * DBW * 4 >= 192;  // accumulators fill the architectural file
+  // the query goes to the accumulation registers when it and the P.V
+  // accumulators would crowd the architectural file
+  static constexpr bool AGPR_Q = NW == 4 && HB * DBW * 4 + HBQ * QR * 4 > 192;
+  static constexpr int KA = NW == 8 ? 1 : 2;         // K-fragment read-ahead in k-steps
   static constexpr int PBYTES = HB * 64 * 16;        // P^T fragments of one tile
-  static constexpr int QBYTES = 4 * HBQ * QL * 1024; // query fragments kept in LDS
-  static constexpr int XBYTES = 16 + G * 4 * 2;      // flags, rescale factors, final m / l
+  static constexpr int QBYTES = NW * HBQ * QL * 1024;  // query fragments kept in LDS
+  static constexpr int XBYTES = 4 * NW + G * 4 * 2;  // flags, rescale factors, final m / l
   static constexpr int LDS_LIMIT = 163840;
   static constexpr int NBUF_MAX = (LDS_LIMIT - PBYTES - QBYTES - XBYTES - 64) / TILE;
   static constexpr int NBUF = NBUF_MAX > 8 ? 8 : NBUF_MAX;  // ring depth
   static constexpr int LDS = NBUF * TILE + PBYTES + QBYTES + XBYTES;
-  static_assert(G % 64 == 0 && G <= 128, "64 or 128 heads per KV head");
-  static_assert(DV % 64 == 0 && DK % 32 == 0, "column blocks must tile the head");
+  static_assert(NW == 4 || NW == 8, "four or eight waves");
+  static_assert(G % 64 == 0 && G <= 128 && HBQ >= 1 && G == 16 * NW * HBQ, "whole head blocks per wave");
+  static_assert(DV % (16 * NW) == 0 && DK % 32 == 0, "column blocks must tile the head");
   static_assert(NBUF >= 3, "ring too shallow");
   static_assert(QL >= 0 && QL < KSTEPS, "some query k-steps stay in registers");
   static_assert(TILE % 16 == 0, "tiles are whole 16-byte chunks");
 };
 
 // One unit: every query head of KV head `kvh` over the pages of one KV range.
-template <int G, int DK, int DV, bool MLA, int QL>
+template <int G, int DK, int DV, bool MLA, int QL, int NW>
 __device__ __forceinline__ void wide_unit(const DecodeArgs &a, const GeomK &gm, const DecReq &rq, const Seg &sg,
                                           char *lds) {
-  using C = WideCfg<G, DK, DV, MLA, QL>;
+  using C = WideCfg<G, DK, DV, MLA, QL, NW>;
+  constexpr int GW = G / NW;  // query heads one wave scores
   const uint32_t kvh = sg.hblk, slot = sg.slot;
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // uniform: lets wave-derived values live in SGPRs
@@ -83,8 +88,8 @@ __device__ __forceinline__ void wide_unit(const DecodeArgs &a, const GeomK &gm, 
   char *const ring = lds;
   char *const pbuf = lds + C::NBUF * C::TILE;
   char *const qbuf = pbuf + C::PBYTES;                                  // [wave][hb][QL][lane] query fragments
-  int *const flags = reinterpret_cast<int *>(qbuf + C::QBYTES);        // [4] rescale needed, per score wave
-  float *const alpha_x = reinterpret_cast<float *>(flags + 4);          // [G] rescale factor of this tile
+  int *const flags = reinterpret_cast<int *>(qbuf + C::QBYTES);        // [NW] rescale needed, per score wave
+  float *const alpha_x = reinterpret_cast<float *>(flags + NW);         // [G] rescale factor of this tile
   float *const ml_x = alpha_x + G;                                      // [G] final: l, after m in alpha_x
 
   // Q^T operand fragments of this wave's score heads: lane holds head
@@ -94,7 +99,7 @@ __device__ __forceinline__ void wide_unit(const DecodeArgs &a, const GeomK &gm, 
   char *const qmine = qbuf + wave * (C::HBQ * QL * 1024);
 #pragma unroll
   for (int hb = 0; hb < C::HBQ; ++hb) {
-    const uint16_t *qrow = a.q + rq.q_off + (uint32_t)(h_kv + (G / 4) * wave + 16 * hb + col) * DK + 8 * quad;
+    const uint16_t *qrow = a.q + rq.q_off + (uint32_t)(h_kv + GW * wave + 16 * hb + col) * DK + 8 * quad;
 #pragma unroll
     for (int c = 0; c < C::QR; ++c) {
       qf[hb][c] = *reinterpret_cast<const bf16x8 *>(qrow + 32 * c);
@@ -136,13 +141,15 @@ __device__ __forceinline__ void wide_unit(const DecodeArgs &a, const GeomK &gm, 
   // write rarely finds the previous group still queued. Lanes on a row's
   // pad fetch the row's last 16 bytes again (same cache line, never read
   // back); lanes past the tile are masked off.
-  constexpr int LBASE = C::NLOADS / 4, LREM = C::NLOADS % 4;
+  constexpr int LBASE = C::NLOADS / NW, LREM = C::NLOADS % NW;
   constexpr int MY_MAX = LBASE + (LREM ? 1 : 0);  // loads of the busiest wave
   constexpr int NGRP = (MY_MAX + 3) / 4;          // M0 groups per wave and tile
   const int my_loads = LBASE + (wave < LREM ? 1 : 0);
   const int my_first = wave * LBASE + min(wave, LREM);
   // per-lane global offsets of this wave's loads, biased for dma_group
-  uint32_t voff[NGRP][4];
+  // (MLA tiles are K rows only, whose offsets fit 16 bits: two per register)
+  constexpr bool PACK = C::TILE_V == 0 && C::TILE <= 65536;
+  uint32_t voff[NGRP][PACK ? 2 : 4];
 #pragma unroll
   for (int g = 0; g < NGRP; ++g)
 #pragma unroll
@@ -158,8 +165,16 @@ __device__ __forceinline__ void wide_unit(const DecodeArgs &a, const GeomK &gm, 
         const int row = o2 / C::VPITCH, w = o2 - row * C::VPITCH;
         gofs = (uint32_t)(P * DK * 2 + row * C::VROW + (w < C::VROW ? w : C::VROW - 16));
       }
-      voff[g][j] = gofs + kDmaBias - 1024u * j;
+      if constexpr (PACK)
+        voff[g][j / 2] = (j & 1) ? (voff[g][j / 2] | (gofs << 16)) : gofs;
+      else
+        voff[g][j] = gofs + kDmaBias - 1024u * j;
     }
+  auto group_offsets = [&](int g, uint32_t (&v)[4]) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      v[j] = PACK ? ((voff[g][j / 2] >> (16 * (j & 1))) & 0xFFFFu) + kDmaBias - 1024u * j : voff[g][PACK ? 0 : j];
+  };
   // Source base of tile k (lowered by kDmaBias) and its slot.
   auto tile_src = [&](int k) -> uint64_t {
     const int sp = k / tpp;
@@ -178,12 +193,14 @@ __device__ __forceinline__ void wide_unit(const DecodeArgs &a, const GeomK &gm, 
     // tile masked off
     const bool tail = C::TILE % 1024 != 0 && first + n == C::NLOADS;
     const int nf = tail ? n - 1 : n;
-    if (nf == 4) dma_group<4>(sb, voff[g], lb);
-    else if (nf == 3) dma_group<3>(sb, voff[g], lb);
-    else if (nf == 2) dma_group<2>(sb, voff[g], lb);
-    else if (nf == 1) dma_group<1>(sb, voff[g], lb);
+    uint32_t vo[4];
+    group_offsets(g, vo);
+    if (nf == 4) dma_group<4>(sb, vo, lb);
+    else if (nf == 3) dma_group<3>(sb, vo, lb);
+    else if (nf == 2) dma_group<2>(sb, vo, lb);
+    else if (nf == 1) dma_group<1>(sb, vo, lb);
     if (tail && (C::NLOADS - 1) * 1024 + lane * 16 < C::TILE) {
-      const uint32_t last[4] = {voff[g][nf] + 1024u * nf, 0u, 0u, 0u};
+      const uint32_t last[4] = {vo[nf] + 1024u * nf, 0u, 0u, 0u};
       dma_group<1>(sb, last, lb + nf * 1024);
     }
   };
@@ -236,7 +253,7 @@ __device__ __forceinline__ void wide_unit(const DecodeArgs &a, const GeomK &gm, 
       // rows past the context may hold stale bytes: zero their V part so that
       // 0 * V stays 0 (their scores are masked to -inf below)
       const int nz = (C::T - valid) * (DV * 2 / 16);
-      for (int i = threadIdx.x; i < nz; i += 256) {
+      for (int i = threadIdx.x; i < nz; i += 64 * NW) {
         const int row = valid + i / (DV * 2 / 16), pc = i % (DV * 2 / 16);
         *reinterpret_cast<uint4 *>(vt + row * C::VPITCH + pc * 16) = make_uint4(0, 0, 0, 0);
       }
@@ -251,38 +268,30 @@ __device__ __forceinline__ void wide_unit(const DecodeArgs &a, const GeomK &gm, 
     {
       const char *kr0 = tb + col * C::KPITCH + quad * 16;
       const char *kr1 = kr0 + 16 * C::KPITCH;
-      // k-steps in pairs; the next pair's K fragments load while this
-      // pair feeds the matrix cores
-      static_assert(C::KSTEPS % 2 == 0, "k-steps in pairs");
-      constexpr int KB = 2, NKB = C::KSTEPS / KB;
-      bf16x8 kf[2][2][KB];
+      // K fragments (k-step c, slice sl) are read KA k-steps ahead of
+      // their products
+      constexpr int KA = C::KA, NK = C::KSTEPS;
+      bf16x8 kf[KA + 1][2];
 #pragma unroll
-      for (int j = 0; j < KB; ++j) {
-        kf[0][0][j] = *reinterpret_cast<const bf16x8 *>(kr0 + 64 * j);
-        kf[0][1][j] = *reinterpret_cast<const bf16x8 *>(kr1 + 64 * j);
+      for (int c = 0; c < KA; ++c) {
+        kf[c][0] = *reinterpret_cast<const bf16x8 *>(kr0 + 64 * c);
+        kf[c][1] = *reinterpret_cast<const bf16x8 *>(kr1 + 64 * c);
       }
 #pragma unroll
-      for (int b = 0; b < NKB; ++b) {
-        if (b + 1 < NKB) {
-#pragma unroll
-          for (int j = 0; j < KB; ++j) {
-            kf[(b + 1) & 1][0][j] = *reinterpret_cast<const bf16x8 *>(kr0 + 64 * ((b + 1) * KB + j));
-            kf[(b + 1) & 1][1][j] = *reinterpret_cast<const bf16x8 *>(kr1 + 64 * ((b + 1) * KB + j));
-          }
+      for (int c = 0; c < NK; ++c) {
+        if (c + KA < NK) {
+          kf[(c + KA) % (KA + 1)][0] = *reinterpret_cast<const bf16x8 *>(kr0 + 64 * (c + KA));
+          kf[(c + KA) % (KA + 1)][1] = *reinterpret_cast<const bf16x8 *>(kr1 + 64 * (c + KA));
         }
-        if (NGRP > 1 && b == NKB / 2 && more) issue_group(kn, sbn, 1);
+        if (NGRP > 1 && c == NK / 2 && more) issue_group(kn, sbn, 1);
 #pragma unroll
-        for (int j = 0; j < KB; ++j) {
-          const int c = b * KB + j;
+        for (int hb = 0; hb < C::HBQ; ++hb) {
+          const bf16x8 qv = c < C::QR ? qf[hb][c < C::QR ? c : 0]
+                                      : *reinterpret_cast<const bf16x8 *>(
+                                            qmine + ((hb * QL + (c - C::QR)) * 64 + lane) * 16);
 #pragma unroll
-          for (int hb = 0; hb < C::HBQ; ++hb) {
-            const bf16x8 qv = c < C::QR ? qf[hb][c < C::QR ? c : 0]
-                                        : *reinterpret_cast<const bf16x8 *>(
-                                              qmine + ((hb * QL + (c - C::QR)) * 64 + lane) * 16);
-#pragma unroll
-            for (int sl = 0; sl < 2; ++sl)
-              s[sl][hb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[b & 1][sl][j], qv, s[sl][hb], 0, 0, 0);
-          }
+          for (int sl = 0; sl < 2; ++sl)
+            s[sl][hb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[c % (KA + 1)][sl], qv, s[sl][hb], 0, 0, 0);
         }
       }
     }
@@ -319,7 +328,7 @@ __device__ __forceinline__ void wide_unit(const DecodeArgs &a, const GeomK &gm, 
         const float al = fast_exp2(m[hb] - mn);
         m[hb] = mn;
         lsum[hb] *= al;
-        if (quad == 0) alpha_x[(G / 4) * wave + 16 * hb + col] = al;
+        if (quad == 0) alpha_x[GW * wave + 16 * hb + col] = al;
       }
     }
     if (lane == 0) flags[wave] = any_bump ? 1 : 0;
@@ -343,8 +352,11 @@ __device__ __forceinline__ void wide_unit(const DecodeArgs &a, const GeomK &gm, 
 
     // ---- rescale this wave's accumulators where a score wave moved its reference
     {
-      const u32x4v fl = *reinterpret_cast<const u32x4v *>(flags);
-      if ((fl.x | fl.y | fl.z | fl.w) != 0) {
+      int fl[NW];
+      int any = 0;
+#pragma unroll
+      for (int w2 = 0; w2 < NW; ++w2) any |= fl[w2] = flags[w2];
+      if (any != 0) {
 #pragma unroll
         for (int hb = 0; hb < C::HB; ++hb) {
           if (fl[hb / C::HBQ]) {
@@ -399,8 +411,8 @@ __device__ __forceinline__ void wide_unit(const DecodeArgs &a, const GeomK &gm, 
   if (quad == 0) {
 #pragma unroll
     for (int hb = 0; hb < C::HBQ; ++hb) {
-      alpha_x[(G / 4) * wave + 16 * hb + col] = m[hb];
-      ml_x[(G / 4) * wave + 16 * hb + col] = lsum[hb];
+      alpha_x[GW * wave + 16 * hb + col] = m[hb];
+      ml_x[GW * wave + 16 * hb + col] = lsum[hb];
     }
   }
   __syncthreads();
@@ -411,7 +423,7 @@ __device__ __forceinline__ void wide_unit(const DecodeArgs &a, const GeomK &gm, 
     const float inv = 1.0f / ml_x[16 * hb + col];
 #pragma unroll
     for (int db = 0; db < C::DBW; ++db) {
-      const int d = (DV / 4) * wave + 16 * db + 4 * quad;
+      const int d = (DV / NW) * wave + 16 * db + 4 * quad;
       const f32x4 v = o[db][hb] * inv;
       if (split) {
         *reinterpret_cast<f32x4 *>(a.ws_o + ((uint64_t)rq.ws_orow + (uint64_t)slot * gm.hq + head) * DV + d) = v;
@@ -426,7 +438,7 @@ __device__ __forceinline__ void wide_unit(const DecodeArgs &a, const GeomK &gm, 
   if (quad == 0) {
 #pragma unroll
     for (int hb = 0; hb < C::HBQ; ++hb) {
-      const uint32_t head = (uint32_t)(h_kv + (G / 4) * wave + 16 * hb + col);
+      const uint32_t head = (uint32_t)(h_kv + GW * wave + 16 * hb + col);
       const float lse = (m[hb] + fast_log2(lsum[hb])) * kLn2;
       if (split)
         a.ws_l[(uint64_t)rq.ws_base + (uint64_t)slot * gm.hq + head] = lse;

@@ -12,20 +12,20 @@
 namespace cp {
 
 template <int V> struct WideVar;
-template <> struct WideVar<kM_MLA_G128> { static constexpr int G = 128, DK = 576, DV = 512, QL = 0; static constexpr bool MLA = true; };
-template <> struct WideVar<kM_D128_G64> { static constexpr int G = 64, DK = 128, DV = 128, QL = 0; static constexpr bool MLA = false; };
-template <> struct WideVar<kM_D128_G128> { static constexpr int G = 128, DK = 128, DV = 128, QL = 0; static constexpr bool MLA = false; };
+template <> struct WideVar<kM_MLA_G128> { static constexpr int G = 128, DK = 576, DV = 512, QL = 0, NW = 8; static constexpr bool MLA = true; };
+template <> struct WideVar<kM_D128_G64> { static constexpr int G = 64, DK = 128, DV = 128, QL = 0, NW = 4; static constexpr bool MLA = false; };
+template <> struct WideVar<kM_D128_G128> { static constexpr int G = 128, DK = 128, DV = 128, QL = 0, NW = 4; static constexpr bool MLA = false; };
 
 // One workgroup of four waves per CU; every request of the launch uses
 // variant V.
 template <int V>
-__global__ __launch_bounds__(256, 1) void decode_wide_kernel(const DecodeArgs a) {
+__global__ __launch_bounds__(64 * WideVar<V>::NW, 1) void decode_wide_kernel(const DecodeArgs a) {
   using W = WideVar<V>;
-  using C = WideCfg<W::G, W::DK, W::DV, W::MLA, W::QL>;
+  using C = WideCfg<W::G, W::DK, W::DV, W::MLA, W::QL, W::NW>;
   __shared__ __attribute__((aligned(16))) char lds[C::LDS];
   __shared__ uint32_t next;
   decode_loop(a, &next, [&](const DecReq &rq, const Seg &sg) {
-    wide_unit<W::G, W::DK, W::DV, W::MLA, W::QL>(a, a.geom[rq.model], rq, sg, lds);
+    wide_unit<W::G, W::DK, W::DV, W::MLA, W::QL, W::NW>(a, a.geom[rq.model], rq, sg, lds);
   });
 }
 
@@ -33,13 +33,13 @@ hipError_t launch_decode_wide(const DecodeArgs &a, int grid, int variant, hipStr
   const dim3 g(grid);
   switch (variant) {
     case kM_MLA_G128:
-      hipLaunchKernelGGL((decode_wide_kernel<kM_MLA_G128>), g, dim3(256), 0, stream, a);
+      hipLaunchKernelGGL((decode_wide_kernel<kM_MLA_G128>), g, dim3(64 * WideVar<kM_MLA_G128>::NW), 0, stream, a);
       return hipGetLastError();
     case kM_D128_G64:
-      hipLaunchKernelGGL((decode_wide_kernel<kM_D128_G64>), g, dim3(256), 0, stream, a);
+      hipLaunchKernelGGL((decode_wide_kernel<kM_D128_G64>), g, dim3(64 * WideVar<kM_D128_G64>::NW), 0, stream, a);
       return hipGetLastError();
     case kM_D128_G128:
-      hipLaunchKernelGGL((decode_wide_kernel<kM_D128_G128>), g, dim3(256), 0, stream, a);
+      hipLaunchKernelGGL((decode_wide_kernel<kM_D128_G128>), g, dim3(64 * WideVar<kM_D128_G128>::NW), 0, stream, a);
       return hipGetLastError();
     default:
       return hipErrorInvalidValue;
