@@ -73,6 +73,7 @@ struct cp_pool {
   float *ws_o = nullptr;
   float *ws_l = nullptr;
   uint64_t ws_o_cap = 0, ws_l_cap = 0;  // floats
+  std::vector<float *> ws_retired;        // outgrown workspaces, freed with the pool
   int num_cus = 256;
 };
 
@@ -147,6 +148,7 @@ cp_status cp_pool_destroy(cp_pool *p) {
     if (p->queue) (void)hipFree(p->queue);
     if (p->ws_o) (void)hipFree(p->ws_o);
     if (p->ws_l) (void)hipFree(p->ws_l);
+    for (float *w : p->ws_retired) (void)hipFree(w);
   }
   delete p;
   return CP_OK;
@@ -443,25 +445,23 @@ int32_t units_per_range(const Geom &g, const GeomK &k) {
 
 cp_status ensure_ws(cp_pool *p, uint64_t o_floats, uint64_t l_floats) {
   if (o_floats <= p->ws_o_cap && l_floats <= p->ws_l_cap) return CP_OK;
-  // Growth is rare; wait for in-flight users of the old workspace.
-  if (hipDeviceSynchronize() != hipSuccess) return fail(CP_EHIP, "synchronise before workspace growth");
-  if (o_floats > p->ws_o_cap) {
-    uint64_t cap = std::max<uint64_t>(o_floats, p->ws_o_cap * 2);
-    if (p->ws_o) (void)hipFree(p->ws_o);
-    p->ws_o = nullptr;
-    p->ws_o_cap = 0;
-    if (hipMalloc((void **)&p->ws_o, cap * 4) != hipSuccess) return fail(CP_ENOMEM, "workspace allocation failed");
-    p->ws_o_cap = cap;
-  }
-  if (l_floats > p->ws_l_cap) {
-    uint64_t cap = std::max<uint64_t>(l_floats, p->ws_l_cap * 2);
-    if (p->ws_l) (void)hipFree(p->ws_l);
-    p->ws_l = nullptr;
-    p->ws_l_cap = 0;
-    if (hipMalloc((void **)&p->ws_l, cap * 4) != hipSuccess) return fail(CP_ENOMEM, "workspace allocation failed");
-    p->ws_l_cap = cap;
-  }
-  return CP_OK;
+  // Growth allocates twice what is asked, so that the slow drift of split
+  // plans as contexts grow rarely repeats it, and keeps the old buffers
+  // until the pool is destroyed: kernels already queued may still use them,
+  // and freeing them here would stall the host until the device drains.
+  auto grow = [&](float **buf, uint64_t *cap, uint64_t need) -> cp_status {
+    if (need <= *cap) return CP_OK;
+    const uint64_t c = std::max<uint64_t>(2 * need, 2 * *cap);
+    float *nb = nullptr;
+    if (hipMalloc((void **)&nb, c * 4) != hipSuccess) return fail(CP_ENOMEM, "workspace allocation failed");
+    if (*buf) p->ws_retired.push_back(*buf);
+    *buf = nb;
+    *cap = c;
+    return CP_OK;
+  };
+  cp_status rc = grow(&p->ws_o, &p->ws_o_cap, o_floats);
+  if (rc) return rc;
+  return grow(&p->ws_l, &p->ws_l_cap, l_floats);
 }
 
 }  // namespace
@@ -583,7 +583,7 @@ cp_status cp_attn_decode_ex(cp_pool *p, int32_t n, const int32_t *req_ids, const
       for (int32_t i : g.idx) {
         const uint64_t c = (uint64_t)gk[model_of(i)].page_cost;
         cost_prefix[i] = (uint32_t)T;
-        T += (kPieceFixedPages + (uint64_t)pages[i]) * c;
+        T += kPieceFixedCost + (uint64_t)pages[i] * c;
         maxc = std::max(maxc, c);
       }
       if (T > 0xFFFFFFFFull) return fail(CP_EINVAL, "batch too large for one launch");
@@ -593,7 +593,7 @@ cp_status cp_attn_decode_ex(cp_pool *p, int32_t n, const int32_t *req_ids, const
       auto owner = [&](uint64_t x) { return (uint32_t)(((x + 1) * W - 1) / T); };
       for (int32_t i : g.idx) {
         // page j of the request sits at C + j c, after the fixed cost
-        const uint64_t c = (uint64_t)gk[model_of(i)].page_cost, C = cost_prefix[i] + kPieceFixedPages * c;
+        const uint64_t c = (uint64_t)gk[model_of(i)].page_cost, C = cost_prefix[i] + kPieceFixedCost;
         const uint32_t w0 = owner(C), w1 = owner(C + (uint64_t)(pages[i] - 1) * c);
         first_worker[i] = (int32_t)w0;
         n_slots[i] = (int32_t)(w1 - w0 + 1);

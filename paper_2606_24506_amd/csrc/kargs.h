@@ -12,11 +12,13 @@ constexpr int kMaxReqPerLaunch = 64;  // requests in one launch (at most one per
 constexpr uint32_t kNoWs = 0xFFFFFFFFu;
 enum : int32_t { kSchedBalanced = 0, kSchedQueue = 1, kSchedGrid = 2 };
 // Balanced schedule: the fixed work of one piece (page-table and query
-// loads, the latency of its first pages, the end merge and the partial
-// write) costs about as much as this many of its pages. Each request's
-// stretch of the cost line starts with that much cost, so a workgroup whose
-// share crosses into another request takes correspondingly fewer pages.
-constexpr uint32_t kPieceFixedPages = 2;
+// loads, the latency of its first pages under a loaded memory system, the
+// end merge and the partial write), in page-cost units (8 KiB of page
+// bytes each): measured at about 23K cycles per piece on the narrow kernel,
+// which streams about 600 cycles per unit. Each request's stretch of the
+// cost line starts with that much cost, so a workgroup whose share crosses
+// into another request takes correspondingly fewer pages.
+constexpr uint32_t kPieceFixedCost = 40;
 
 // Decode code paths (GeomK::variant), chosen per model by the host.
 //   Vector path (0-7): wavefront reductions; heads per block (16 or 8) and
