@@ -248,9 +248,10 @@ typedef struct {
   int32_t schedule; /* cp_schedule; opts == NULL means CP_SCHED_BALANCED */
   int32_t path;     /* cp_path */
   int32_t reserved0;
-  /* Optional hipEvent_t handles recorded on the stream immediately before
-   * the first and after the last attention kernel of the call (the split
-   * merge is not included), for timing. */
+  /* Optional hipEvent_t handles (created with timing enabled) that take
+   * the start time of the first and the end time of the last attention
+   * kernel of the call, from those launches themselves (no separate
+   * marker in the stream); the split merge is not included. */
   void *ev_begin;
   void *ev_end;
 } cp_decode_opts;

@@ -17,8 +17,10 @@
 namespace cp {
 hipError_t launch_append(const AppendArgs &a, hipStream_t stream);
 hipError_t launch_gather(const GatherArgs &a, hipStream_t stream);
-hipError_t launch_decode(const DecodeArgs &a, int grid, uint32_t mask, hipStream_t stream);
-hipError_t launch_decode_wide(const DecodeArgs &a, int grid, int variant, hipStream_t stream);
+hipError_t launch_decode(const DecodeArgs &a, int grid, uint32_t mask, hipStream_t stream, hipEvent_t ev0,
+                         hipEvent_t ev1);
+hipError_t launch_decode_wide(const DecodeArgs &a, int grid, int variant, hipStream_t stream, hipEvent_t ev0,
+                              hipEvent_t ev1);
 int decode_wgs_per_cu(uint32_t mask);
 int narrow_streams(int variant);
 hipError_t launch_merge(const MergeArgs &a, hipStream_t stream);
@@ -663,11 +665,11 @@ cp_status cp_attn_decode_ex(cp_pool *p, int32_t n, const int32_t *req_ids, const
     rc = ensure_ws(p, ws_floats, ws_rows);
     if (rc) return rc;
   }
-  if (o.ev_begin) {
-    hipError_t e = hipEventRecord((hipEvent_t)o.ev_begin, s);
-    if (e != hipSuccess) return hip_fail(e, "event record");
-  }
-  for (const Group &g : groups) {
+  // The caller's events take the start of the first decode launch and the
+  // end of the last one (timestamps of the launches themselves, no marker
+  // packets between them).
+  for (size_t gi = 0; gi < groups.size(); ++gi) {
+    const Group &g = groups[gi];
     DecodeArgs a{};
     a.pool = p->dev_pool;
     a.pte = p->dev_pte;
@@ -699,12 +701,11 @@ cp_status cp_attn_decode_ex(cp_pool *p, int32_t n, const int32_t *req_ids, const
     }
     if (g.grid > 0xFFFF && o.schedule == CP_SCHED_BALANCED) return fail(CP_EINVAL, "too many workers");
     const int v0 = __builtin_ctz(g.mask);
-    hipError_t e = is_wide_variant(v0) ? launch_decode_wide(a, g.grid, v0, s) : launch_decode(a, g.grid, g.mask, s);
+    const hipEvent_t ev0 = gi == 0 ? (hipEvent_t)o.ev_begin : nullptr;
+    const hipEvent_t ev1 = gi + 1 == groups.size() ? (hipEvent_t)o.ev_end : nullptr;
+    hipError_t e = is_wide_variant(v0) ? launch_decode_wide(a, g.grid, v0, s, ev0, ev1)
+                                       : launch_decode(a, g.grid, g.mask, s, ev0, ev1);
     if (e != hipSuccess) return hip_fail(e, "decode launch");
-  }
-  if (o.ev_end) {
-    hipError_t e = hipEventRecord((hipEvent_t)o.ev_end, s);
-    if (e != hipSuccess) return hip_fail(e, "event record");
   }
 
   // Merge launches for split requests.

@@ -7,6 +7,7 @@
 //   GQA/MQA  head-major [Hkv][ K: P x d | V: P x d ] bf16, so the K (or V)
 //            rows of one KV head inside one page are one contiguous block.
 // A page starts at pool + (pte << 8).
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include "decode_mfma.h"
@@ -334,11 +335,13 @@ constexpr uint32_t kAllNarrow =
 // Picks the kernel instantiation that covers `mask`. Returns
 // hipErrorInvalidValue for a set no instantiation covers (the host keeps
 // variants of different workgroup sizes in separate launches).
-hipError_t launch_decode(const DecodeArgs &a, int grid, uint32_t mask, hipStream_t stream) {
+// ev0 / ev1 (may be null) take the start and end time of the launch.
+hipError_t launch_decode(const DecodeArgs &a, int grid, uint32_t mask, hipStream_t stream, hipEvent_t ev0,
+                         hipEvent_t ev1) {
   const dim3 g(grid);
 #define CP_L(M)                                                                       \
   case M:                                                                             \
-    hipLaunchKernelGGL((decode_kernel<M>), g, dim3(64 * kernel_waves<M>()), 0, stream, a); \
+    hipExtLaunchKernelGGL((decode_kernel<M>), g, dim3(64 * kernel_waves<M>()), 0, stream, ev0, ev1, 0, a); \
     return hipGetLastError();
   switch (mask) {
     CP_L(vbit(kV16x8)) CP_L(vbit(kV16x4)) CP_L(vbit(kV16x2)) CP_L(vbit(kV16x1))
@@ -350,11 +353,11 @@ hipError_t launch_decode(const DecodeArgs &a, int grid, uint32_t mask, hipStream
   }
 #undef CP_L
   if ((mask & ~kValuMask) == 0) {
-    hipLaunchKernelGGL((decode_kernel<kValuMask>), g, dim3(256), 0, stream, a);
+    hipExtLaunchKernelGGL((decode_kernel<kValuMask>), g, dim3(256), 0, stream, ev0, ev1, 0, a);
     return hipGetLastError();
   }
   if ((mask & ~kAllNarrow) == 0) {
-    hipLaunchKernelGGL((decode_kernel<kAllNarrow>), g, dim3(64 * kNarrowWaves), 0, stream, a);
+    hipExtLaunchKernelGGL((decode_kernel<kAllNarrow>), g, dim3(64 * kNarrowWaves), 0, stream, ev0, ev1, 0, a);
     return hipGetLastError();
   }
   return hipErrorInvalidValue;

@@ -3,6 +3,7 @@
 // all 512 registers of a lane: its 256 P.V accumulators take the
 // architectural file and the register allocator parks the query fragments
 // and other long-lived values in the accumulation file.
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include "decode_wide.h"
@@ -29,17 +30,19 @@ __global__ __launch_bounds__(64 * WideVar<V>::NW, 1) void decode_wide_kernel(con
   });
 }
 
-hipError_t launch_decode_wide(const DecodeArgs &a, int grid, int variant, hipStream_t stream) {
+// ev0 / ev1 (may be null) take the start and end time of the launch.
+hipError_t launch_decode_wide(const DecodeArgs &a, int grid, int variant, hipStream_t stream, hipEvent_t ev0,
+                              hipEvent_t ev1) {
   const dim3 g(grid);
   switch (variant) {
     case kM_MLA_G128:
-      hipLaunchKernelGGL((decode_wide_kernel<kM_MLA_G128>), g, dim3(64 * WideVar<kM_MLA_G128>::NW), 0, stream, a);
+      hipExtLaunchKernelGGL((decode_wide_kernel<kM_MLA_G128>), g, dim3(64 * WideVar<kM_MLA_G128>::NW), 0, stream, ev0, ev1, 0, a);
       return hipGetLastError();
     case kM_D128_G64:
-      hipLaunchKernelGGL((decode_wide_kernel<kM_D128_G64>), g, dim3(64 * WideVar<kM_D128_G64>::NW), 0, stream, a);
+      hipExtLaunchKernelGGL((decode_wide_kernel<kM_D128_G64>), g, dim3(64 * WideVar<kM_D128_G64>::NW), 0, stream, ev0, ev1, 0, a);
       return hipGetLastError();
     case kM_D128_G128:
-      hipLaunchKernelGGL((decode_wide_kernel<kM_D128_G128>), g, dim3(64 * WideVar<kM_D128_G128>::NW), 0, stream, a);
+      hipExtLaunchKernelGGL((decode_wide_kernel<kM_D128_G128>), g, dim3(64 * WideVar<kM_D128_G128>::NW), 0, stream, ev0, ev1, 0, a);
       return hipGetLastError();
     default:
       return hipErrorInvalidValue;
