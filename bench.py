@@ -215,10 +215,11 @@ def main():
     t_enq = time.perf_counter() - t0
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    # Kernel-timing pass: the next K steps, with HIP events recorded on the
-    # launch stream right around each decode kernel (inside the library
-    # call). An event record makes the stream idle for a few microseconds,
-    # so these steps are not part of the throughput figure.
+    # Kernel-timing pass: the next K steps, with HIP events taken by the
+    # decode launches themselves on the launch stream (start of the first,
+    # end of the last attention kernel of each call). Launching with events
+    # costs the host tens of microseconds per call, enough to leave the GPU
+    # waiting, so these steps are not part of the throughput figure.
     for i in range(args.steps):
         step(args.warmup + args.steps + i, ev[i])
     torch.cuda.synchronize()
