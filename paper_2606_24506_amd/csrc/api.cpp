@@ -395,7 +395,15 @@ cp_status cp_kv_gather(cp_pool *p, int32_t req_id, int64_t start, int64_t n_tok,
 namespace {
 
 // Vector-path variant for a model: heads per block and V values per lane.
-void choose_valu(const Geom &g, GeomK *k) {
+void choose_valu(const Geom &g, GeomK *k, int32_t P) {
+  // GQA/MHA groups of 1 to 4 heads with head_dim 64 or 128 take the
+  // small-group kernel (one KV head per unit)
+  if (g.kind == kGQA && g.g <= 4 && (g.head_dim == 64 || g.head_dim == 128) && P % 16 == 0) {
+    const int gi = g.g == 1 ? 0 : g.g == 2 ? 1 : 2;  // 3 heads run as 4, one padded
+    k->variant = (g.head_dim == 64 ? kS_G1_D64 : kS_G1_D128) + gi;
+    k->nb = 1;
+    return;
+  }
   const int hb = g.g > 8 ? 16 : 8;
   const int dpl = g.d_v / 64;
   int v = 0;
@@ -502,7 +510,7 @@ cp_status cp_attn_decode_ex(cp_pool *p, int32_t n, const int32_t *req_ids, const
       gk[m].variant = mv;
       gk[m].nb = mv == kM_MLA_G32 ? 2 : 1;  // units of 16 heads per KV range
     } else {
-      choose_valu(g, &gk[m]);
+      choose_valu(g, &gk[m], P);
     }
     // relative work of one page: its bytes, times the head blocks that each
     // reread it on the MLA vector path
@@ -536,7 +544,8 @@ cp_status cp_attn_decode_ex(cp_pool *p, int32_t n, const int32_t *req_ids, const
   // share another, and each wide variant has a kernel of its own
   auto wclass = [&](int32_t i) {
     const int v = gk[model_of(i)].variant;
-    return is_wide_variant(v) ? v : (v >= kMatrixFirst ? 1 : 0);
+    // (launch classes: vector, narrow matrix, small-group vector, each wide variant)
+    return is_wide_variant(v) ? v : v >= kMatrixFirst ? 1 : (v >= kS_G1_D64 && v <= kS_G4_D128) ? 2 : 0;
   };
 
   // Launch groups: requests whose kernels share a workgroup size, at most

@@ -22,7 +22,9 @@ constexpr uint32_t kPieceFixedCost = 40;
 
 // Decode code paths (GeomK::variant), chosen per model by the host.
 //   Vector path (0-7): wavefront reductions; heads per block (16 or 8) and
-//     V values per lane (8, 4, 2, 1).
+//     V values per lane (8, 4, 2, 1); any geometry.
+//   Small-group vector path (8-13): wavefront reductions for GQA/MHA with
+//     1, 2 or 4 query heads per KV head and head_dim 64 or 128.
 //   Narrow matrix path (16, 17, 19, 20, 23): 8, 16 or 32 query heads per KV
 //     head (MLA latent head, or head_dim 128).
 //   Wide matrix path (18, 21, 22): 64 or 128 query heads per KV head; its
@@ -30,6 +32,7 @@ constexpr uint32_t kPieceFixedCost = 40;
 //     columns).
 enum : int32_t {
   kV16x8 = 0, kV16x4, kV16x2, kV16x1, kV8x8, kV8x4, kV8x2, kV8x1,
+  kS_G1_D64 = 8, kS_G2_D64, kS_G4_D64, kS_G1_D128, kS_G2_D128, kS_G4_D128,
   kM_MLA_G16 = 16, kM_MLA_G32, kM_MLA_G128, kM_D128_G16, kM_D128_G32, kM_D128_G64, kM_D128_G128, kM_D128_G8
 };
 constexpr bool is_wide_variant(int v) { return v == kM_MLA_G128 || v == kM_D128_G64 || v == kM_D128_G128; }

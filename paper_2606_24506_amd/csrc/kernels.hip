@@ -12,6 +12,7 @@
 
 #include "decode_mfma.h"
 #include "decode_narrow.h"
+#include "decode_small.h"
 #include "device_common.h"
 #include "kargs.h"
 #include "schedule.h"
@@ -274,11 +275,25 @@ constexpr int narrow_lds() { return NarrowCfgOf<V>::LDS; }
 
 constexpr bool has(uint32_t mask, int v) { return (mask >> v) & 1u; }
 constexpr uint32_t kValuMask = 0xFFu;
+constexpr uint32_t kSmallMask = 0x3F00u;  // variants 8-13
+
+template <int V> struct SmallVar;
+template <> struct SmallVar<kS_G1_D64> { static constexpr int G = 1, D = 64; };
+template <> struct SmallVar<kS_G2_D64> { static constexpr int G = 2, D = 64; };
+template <> struct SmallVar<kS_G4_D64> { static constexpr int G = 4, D = 64; };
+template <> struct SmallVar<kS_G1_D128> { static constexpr int G = 1, D = 128; };
+template <> struct SmallVar<kS_G2_D128> { static constexpr int G = 2, D = 128; };
+template <> struct SmallVar<kS_G4_D128> { static constexpr int G = 4, D = 128; };
+template <int V>
+constexpr int small_lds() { return SmallCfg<SmallVar<V>::G, SmallVar<V>::D>::LDS; }
 
 // LDS bytes of a kernel covering the variant set `mask`.
 constexpr int kernel_lds_bytes(uint32_t mask) {
   int b = 16;
   if (mask & kValuMask) b = kLdsFloats * 4 > b ? kLdsFloats * 4 : b;
+#define CP_S(V) if (has(mask, V) && small_lds<V>() > b) b = small_lds<V>();
+  CP_S(kS_G1_D64) CP_S(kS_G2_D64) CP_S(kS_G4_D64) CP_S(kS_G1_D128) CP_S(kS_G2_D128) CP_S(kS_G4_D128)
+#undef CP_S
 #define CP_B(V) if (has(mask, V) && narrow_lds<V>() > b) b = narrow_lds<V>();
   CP_B(kM_MLA_G16) CP_B(kM_MLA_G32) CP_B(kM_D128_G8) CP_B(kM_D128_G16) CP_B(kM_D128_G32)
 #undef CP_B
@@ -298,6 +313,16 @@ __device__ __forceinline__ void run_seg(const DecodeArgs &a, const DecReq &rq, c
   CP_VCASE(kV16x8, 16, 8) CP_VCASE(kV16x4, 16, 4) CP_VCASE(kV16x2, 16, 2) CP_VCASE(kV16x1, 16, 1)
   CP_VCASE(kV8x8, 8, 8) CP_VCASE(kV8x4, 8, 4) CP_VCASE(kV8x2, 8, 2) CP_VCASE(kV8x1, 8, 1)
 #undef CP_VCASE
+#define CP_SCASE(V)                                                                          \
+  if constexpr (has(MASK, V)) {                                                              \
+    if (gm.variant == V) {                                                                   \
+      small_unit<SmallVar<V>::G, SmallVar<V>::D>(a, gm, rq, sg, reinterpret_cast<float *>(lds)); \
+      return;                                                                                \
+    }                                                                                        \
+  }
+  CP_SCASE(kS_G1_D64) CP_SCASE(kS_G2_D64) CP_SCASE(kS_G4_D64) CP_SCASE(kS_G1_D128) CP_SCASE(kS_G2_D128)
+  CP_SCASE(kS_G4_D128)
+#undef CP_SCASE
 #define CP_NCASE(V)                                                                          \
   if constexpr (has(MASK, V)) {                                                              \
     if (gm.variant == V) {                                                                   \
@@ -315,11 +340,12 @@ __device__ __forceinline__ void run_seg(const DecodeArgs &a, const DecReq &rq, c
 // Vector variants run four waves per workgroup, narrow matrix variants
 // eight; the host never mixes the two families in one launch.
 template <uint32_t MASK>
-constexpr int kernel_waves() { return (MASK & kValuMask) ? 4 : kNarrowWaves; }
+constexpr int kernel_waves() { return (MASK & (kValuMask | kSmallMask)) ? 4 : kNarrowWaves; }
 
 template <uint32_t MASK>
 __global__ __launch_bounds__(64 * kernel_waves<MASK>()) void decode_kernel(const DecodeArgs a) {
-  static_assert(!((MASK & kValuMask) && (MASK & ~kValuMask)), "vector and matrix variants launch separately");
+  static_assert(!((MASK & kValuMask) && (MASK & ~kValuMask)) && !((MASK & kSmallMask) && (MASK & ~kSmallMask)),
+                "vector, small-group and matrix variants launch separately");
   __shared__ __attribute__((aligned(16))) char lds[kernel_lds_bytes(MASK)];
   __shared__ uint32_t next;
   decode_loop(a, &next, [&](const DecReq &rq, const Seg &sg) { run_seg<MASK>(a, rq, sg, lds); });
@@ -349,11 +375,17 @@ hipError_t launch_decode(const DecodeArgs &a, int grid, uint32_t mask, hipStream
     CP_L(vbit(kM_MLA_G16)) CP_L(vbit(kM_MLA_G32)) CP_L(vbit(kM_D128_G16)) CP_L(vbit(kM_D128_G32))
     CP_L(vbit(kM_D128_G8))
     CP_L(kMixedSmall)
+    CP_L(vbit(kS_G1_D64)) CP_L(vbit(kS_G2_D64)) CP_L(vbit(kS_G4_D64)) CP_L(vbit(kS_G1_D128)) CP_L(vbit(kS_G2_D128))
+    CP_L(vbit(kS_G4_D128))
     default: break;
   }
 #undef CP_L
   if ((mask & ~kValuMask) == 0) {
     hipExtLaunchKernelGGL((decode_kernel<kValuMask>), g, dim3(256), 0, stream, ev0, ev1, 0, a);
+    return hipGetLastError();
+  }
+  if ((mask & ~kSmallMask) == 0) {
+    hipExtLaunchKernelGGL((decode_kernel<kSmallMask>), g, dim3(256), 0, stream, ev0, ev1, 0, a);
     return hipGetLastError();
   }
   if ((mask & ~kAllNarrow) == 0) {
@@ -378,6 +410,9 @@ int narrow_streams(int variant) {
 
 // Workgroups of one kernel that fit on a CU at once (LDS-bound).
 int decode_wgs_per_cu(uint32_t mask) {
+  // small-group vector kernels: two workgroups (eight waves) per CU, so
+  // that each SIMD has a second wave to issue while one waits on memory
+  if ((mask & kSmallMask) && !(mask & ~kSmallMask)) return 2;
   int b = 16;
   if (mask & 0xFFu) b = kLdsFloats * 4;
 #define CP_B(V) if (has(mask, V) && narrow_lds<V>() > b) b = narrow_lds<V>();

@@ -130,7 +130,8 @@ def test_balanced_schedule_rejects_forced_splits():
 
 
 VARIANT_MODELS = [("mla16", 700), ("mla32", 333), ("mla128", 290), ("mqa16", 515), ("mqa32", 190),
-                  ("gqa128x2", 257), ("mqa128", 129), ("gqa32x4", 450), ("gqa8x8d64", 97)]
+                  ("gqa128x2", 257), ("mqa128", 129), ("gqa32x4", 450), ("gqa8x8d64", 97),
+                  ("gqa32x8", 611), ("gqa16x8", 77), ("gqa24x8", 301), ("gqa16x4d64", 1043)]
 
 
 @pytest.mark.parametrize("schedule,splits", SCHEDULES)

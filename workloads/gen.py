@@ -75,6 +75,11 @@ MODELS: Dict[str, ModelSpec] = {
     "gqa128x2": ModelSpec("gqa128x2", "gqa", 128, 2, head_dim=128, scale=1.0 / math.sqrt(128.0)),
     "mqa128": ModelSpec("mqa128", "gqa", 128, 1, head_dim=128, scale=1.0 / math.sqrt(128.0)),
     "gqa8x8d64": ModelSpec("gqa8x8d64", "gqa", 8, 8, head_dim=64, scale=1.0 / math.sqrt(64.0)),
+    # Llama-style GQA with four query heads per KV head (the wavefront-reduction path).
+    "gqa32x8": ModelSpec("gqa32x8", "gqa", 32, 8, head_dim=128, scale=1.0 / math.sqrt(128.0)),
+    "gqa16x8": ModelSpec("gqa16x8", "gqa", 16, 8, head_dim=128, scale=1.0 / math.sqrt(128.0)),
+    "gqa24x8": ModelSpec("gqa24x8", "gqa", 24, 8, head_dim=128, scale=1.0 / math.sqrt(128.0)),
+    "gqa16x4d64": ModelSpec("gqa16x4d64", "gqa", 16, 4, head_dim=64, scale=1.0 / math.sqrt(64.0)),
 }
 
 
