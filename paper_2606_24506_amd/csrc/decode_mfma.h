@@ -16,6 +16,16 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
 constexpr float kLazy = 8.0f;  // log2 headroom before the softmax reference moves
 
+// Instruction classes of __builtin_amdgcn_sched_group_barrier.
+constexpr int kSgValu = 0x2, kSgMfma = 0x8, kSgDsRead = 0x100, kSgDsWrite = 0x200, kSgTrans = 0x400;
+
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+// Two floats rounded to bf16 (nearest even), packed low | high << 16.
+CP_DEV uint32_t pack_bf16x2(float lo, float hi) {
+  const bf16x2 v = {(__bf16)lo, (__bf16)hi};
+  return __builtin_bit_cast(uint32_t, v);
+}
+
 // Direct HBM -> LDS loads are issued through inline asm, so the compiler
 // does not put a full vmcnt wait before every LDS read; completion is
 // awaited with wait_vm<N>() below. KV is streamed once per call, so the

@@ -1,18 +1,17 @@
-// Matrix-core decode path for models with 64 or more query heads per KV
-// head (DeepSeek-V3-shaped MLA with 128 heads on one latent head; MQA and
-// GQA groups of 64 or 128). There the per-token work is a dense
-// contraction of about 240 flop per KV byte, so the kernel must keep the
-// matrix cores near half of their peak while streaming KV at HBM speed.
+// Generic matrix-core decode path for models with 64 or 128 query heads per
+// KV head and separate K and V rows (MQA / GQA groups of 64 or 128 with
+// head_dim 128). The 128-head MLA geometry has its own pipelined kernel
+// (decode_mla.h). Per token the work is a dense contraction, so the kernel
+// keeps the matrix cores busy while streaming KV at HBM speed.
 //
-// One workgroup of four waves (one per SIMD) shares a ring of NBUF tiles of
-// T = 32 tokens that stream HBM -> LDS by direct, non-temporal loads. Per
-// tile:
-//   scores   wave w owns query heads [w G/4, (w+1) G/4): for them it computes
-//            S^T[t][h] = sum_d K[t][d] Q[h][d] (mfma 16x16x32 bf16, K rows
-//            from LDS as the A operand, Q^T in registers as B), the fp32
-//            online softmax (lazily moved reference maximum), and publishes
-//            P^T as bf16 operand fragments;
-//   P.V      wave w owns V columns [w DV/4, (w+1) DV/4) for every head:
+// One workgroup of NW waves shares a ring of NBUF tiles of T = 32 tokens
+// that stream HBM -> LDS by direct, non-temporal loads. Per tile:
+//   scores   wave w owns query heads [w G/NW, (w+1) G/NW): for them it
+//            computes S^T[t][h] = sum_d K[t][d] Q[h][d] (mfma 16x16x32 bf16,
+//            K rows from LDS as the A operand, Q^T in registers as B), the
+//            fp32 online softmax (lazily moved reference maximum), and
+//            publishes P^T as bf16 operand fragments;
+//   P.V      wave w owns V columns [w DV/NW, (w+1) DV/NW) for every head:
 //            O^T[d][h] += sum_t V^T[d][t] P^T[t][h] over the tile's 32 tokens
 //            with one mfma 16x16x32 per (column block, head block). The K
 //            index of that product runs over the 32 tokens in the order
@@ -20,11 +19,9 @@
 //            how the two 16-token score accumulators hold them, so the score
 //            lanes' P values are the B operand as they stand and V^T comes
 //            from two LDS transpose reads.
-// Every K byte is read from LDS once per score wave and every V byte once,
-// the matrix work of the two phases is the same in every wave, and no wave
-// redoes another's work. Scores and P.V of one tile are separated by a
-// barrier (P and the rescale factors cross waves); a second barrier at the
-// top of the next tile releases the ring slot.
+// Scores and P.V of one tile are separated by a barrier (P and the rescale
+// factors cross waves); a second barrier at the top of the next tile
+// releases the ring slot.
 #pragma once
 
 #include "decode_mfma.h"

@@ -1,11 +1,11 @@
 // gfx950 decode kernels of the wide matrix path (64 or 128 query heads per
-// KV head), one instantiation per geometry. The 128-head MLA instance needs
-// all 512 registers of a lane: its 256 P.V accumulators take the
-// architectural file and the register allocator parks the query fragments
-// and other long-lived values in the accumulation file.
+// KV head): the pipelined 128-head MLA kernel (decode_mla.h) and one
+// instantiation of the generic wide kernel (decode_wide.h) per head_dim-128
+// geometry.
 #include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
+#include "decode_mla.h"
 #include "decode_wide.h"
 #include "kargs.h"
 #include "schedule.h"
@@ -13,9 +13,15 @@
 namespace cp {
 
 template <int V> struct WideVar;
-template <> struct WideVar<kM_MLA_G128> { static constexpr int G = 128, DK = 576, DV = 512, QL = 0, NW = 8; static constexpr bool MLA = true; };
 template <> struct WideVar<kM_D128_G64> { static constexpr int G = 64, DK = 128, DV = 128, QL = 0, NW = 4; static constexpr bool MLA = false; };
 template <> struct WideVar<kM_D128_G128> { static constexpr int G = 128, DK = 128, DV = 128, QL = 0, NW = 4; static constexpr bool MLA = false; };
+
+// 128-head MLA: one workgroup of eight waves per CU.
+__global__ __launch_bounds__(64 * MlaCfg::NW, 1) void decode_mla_kernel(const DecodeArgs a) {
+  __shared__ __attribute__((aligned(16))) char lds[MlaCfg::LDS];
+  __shared__ uint32_t next;
+  decode_loop(a, &next, [&](const DecReq &rq, const Seg &sg) { mla_unit<true>(a, a.geom[rq.model], rq, sg, lds); });
+}
 
 // One workgroup of four waves per CU; every request of the launch uses
 // variant V.
@@ -36,7 +42,7 @@ hipError_t launch_decode_wide(const DecodeArgs &a, int grid, int variant, hipStr
   const dim3 g(grid);
   switch (variant) {
     case kM_MLA_G128:
-      hipExtLaunchKernelGGL((decode_wide_kernel<kM_MLA_G128>), g, dim3(64 * WideVar<kM_MLA_G128>::NW), 0, stream, ev0, ev1, 0, a);
+      hipExtLaunchKernelGGL(decode_mla_kernel, g, dim3(64 * MlaCfg::NW), 0, stream, ev0, ev1, 0, a);
       return hipGetLastError();
     case kM_D128_G64:
       hipExtLaunchKernelGGL((decode_wide_kernel<kM_D128_G64>), g, dim3(64 * WideVar<kM_D128_G64>::NW), 0, stream, ev0, ev1, 0, a);
