@@ -19,10 +19,10 @@
 // Software pipeline: iteration k computes the scores and softmax of tile k
 // and the P.V product of tile k-1, with one workgroup barrier per tile.
 // P^T and the rescale factors are double-buffered by tile parity, so a wave
-// may publish tile k's while another still multiplies tile k-1's. Each wave
-// of the second half does its P.V before its scores, so the two waves of a
-// SIMD rarely sit in their softmax at the same time and the matrix core
-// always has an instruction to issue.
+// may publish tile k's while another still multiplies tile k-1's, and the two
+// waves of a SIMD drift apart within the iteration: one's softmax and LDS
+// waits are the other's matrix-core issue slots. (Fixed opposite orders for
+// the two waves, and wave priorities, measured no better.)
 //
 // LDS (160 KiB): a ring of four value tiles (32 rows of 1024 bytes), a ring
 // of three rotary tiles (32 rows of 128 bytes: the rotary part is only read
@@ -88,7 +88,6 @@ CP_DEV LaneIds lane_ids(int tid) {
   return LaneIds{lane, lane & 15, lane >> 4};
 }
 
-template <bool STAGGER>
 __device__ __forceinline__ void mla_unit(const DecodeArgs &a, const GeomK &gm, const DecReq &rq, const Seg &sg,
                                          char *lds) {
   using C = MlaCfg;
@@ -101,8 +100,6 @@ __device__ __forceinline__ void mla_unit(const DecodeArgs &a, const GeomK &gm, c
   const int P = gm.page_tokens;  // the host routes only pages of a multiple of 32 tokens here
   const int tpp = P / T;
   const int h0 = (int)sg.hblk * C::G;  // first query head of the (single) KV head
-  // second-half waves multiply the previous tile before scoring the current one
-  const bool late = STAGGER && wave >= NW / 2;
 
   char *const vring = lds;
   char *const rring = lds + C::OFF_R;
@@ -281,12 +278,6 @@ __device__ __forceinline__ void mla_unit(const DecodeArgs &a, const GeomK &gm, c
     const uint64_t sbn = more ? tile_src(kn) : 0;
     if (more) issue_value(L, kn, sbn, 0);
 
-    PvRegs pr;
-    if (late && k >= 1) {
-      pv_load(L, k - 1, pr);
-      pv_mma(L, k - 1, pr);
-    }
-
     if (k < ntiles) {
       char *vt = vring + (k % C::NM) * C::MSLOT;
       const int t0 = (int)((pg_begin + (uint32_t)(k / tpp)) * P) + (k % tpp) * T;
@@ -374,7 +365,8 @@ __device__ __forceinline__ void mla_unit(const DecodeArgs &a, const GeomK &gm, c
       for (int b = 0; b < 4; ++b) kva[b] = vbase + ((kva[b] - vbase + C::MSLOT) & (C::NM * C::MSLOT - 1));
     }
 
-    if (!late && k >= 1) {
+    if (k >= 1) {
+      PvRegs pr;
       pv_load(L, k - 1, pr);
       pv_mma(L, k - 1, pr);
     }
