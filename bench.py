@@ -50,6 +50,8 @@ def parse():
     ap.add_argument("--path", type=int, default=0, help="0 auto, 1 vector, 2 matrix cores")
     ap.add_argument("--splits", type=int, default=0, help="forced KV ranges per request (queue/grid schedules)")
     ap.add_argument("--schedule", type=int, default=0, help="0 balanced, 1 work queue, 2 one workgroup per unit")
+    ap.add_argument("--unfused", action="store_true",
+                    help="step as cp_kv_append + cp_attn_decode_ex instead of cp_attn_decode_step")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="target CPU time of the oracle sample")
     ap.add_argument("--copy-mib", type=int, default=0,
@@ -189,11 +191,14 @@ def main():
 
     def step(i, evs=None):
         ld = lds[i % layers]
-        ld.pool.append(ld.req_ids, ones, new_rows, stream)
         opts = dict(num_splits=args.splits, path=args.path, schedule=args.schedule)
         if evs is not None:
             opts.update(ev_begin=evs[0].cuda_event, ev_end=evs[1].cuda_event)
-        ld.pool.decode(ld.req_ids, ld.q, ld.out, ld.lse, stream, **opts)
+        if args.unfused:
+            ld.pool.append(ld.req_ids, ones, new_rows, stream)
+            ld.pool.decode(ld.req_ids, ld.q, ld.out, ld.lse, stream, **opts)
+        else:
+            ld.pool.decode_step(ld.req_ids, ones, new_rows, ld.q, ld.out, ld.lse, stream, **opts)
 
     for i in range(args.warmup):
         step(i)
@@ -258,7 +263,8 @@ def main():
             "context_tokens": int(sum(ctx0[0])),
             "kv_bytes_per_step": int(kv_bytes),
             "layers_cycled": layers,
-            "step": "cp_kv_append (1 token/request) + cp_attn_decode",
+            "step": ("cp_kv_append (1 token/request) + cp_attn_decode" if args.unfused
+                     else "cp_attn_decode_step: 1 appended token/request + decode, append fused into the launch"),
             "path": ["auto", "vector", "matrix"][args.path],
             "schedule": ["balanced", "queue", "grid"][args.schedule],
         },

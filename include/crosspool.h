@@ -260,6 +260,31 @@ typedef struct {
 cp_status cp_attn_decode_ex(cp_pool *pool, int32_t n, const int32_t *req_ids, const void *q, void *out, float *lse,
                             void *hip_stream, const cp_decode_opts *opts);
 
+/* One decode step with single-token appends: the effect of cp_kv_append(pool,
+ * n, req_ids, n_new, rows, hip_stream) followed by cp_attn_decode_ex(pool, n,
+ * req_ids, q, out, lse, hip_stream, opts), with the same arguments, layouts
+ * and results (out and lse bit-identical), but without the append launch
+ * and the page-table copy: the attention launches write the new rows and
+ * page-table entries themselves. This lowers the per-token host control of
+ * the pool's decode step into the device launch (Section 4, control
+ * lowering).
+ *
+ *   n_new   host, n entries, each 0 or 1 (a decode step appends at most the
+ *           token just generated).
+ *   rows    device, the new logical rows packed in call order (requests with
+ *           n_new = 0 contribute none); may be NULL when every n_new is 0.
+ *
+ * Pages for the new tokens are allocated on the host as in cp_kv_append; the
+ * entry of a new page is passed to the launch, and every workgroup that reads
+ * a request's last page writes that entry and the new row before reading it.
+ * Errors: those of cp_kv_append and cp_attn_decode_ex, plus CP_EINVAL for an
+ * n_new other than 0 or 1. Argument and capacity checks run before any state
+ * changes; if the attention launch fails once pages are allocated, the rows
+ * are still appended (as by cp_kv_append) and the error is returned. */
+cp_status cp_attn_decode_step(cp_pool *pool, int32_t n, const int32_t *req_ids, const int32_t *n_new,
+                              const void *rows, const void *q, void *out, float *lse, void *hip_stream,
+                              const cp_decode_opts *opts);
+
 /* Copy logical rows [start, start + n_tok) of one request out of the pool
  * into dst (device, n_tok * row_elems bf16), through the same page-table
  * translation that decode uses. Bit-exact inverse of cp_kv_append.

@@ -61,6 +61,16 @@ struct DeviceGuard {
   }
 };
 
+
+// One fused append of cp_attn_decode_step, per request in call order.
+struct AppendPlan {
+  uint8_t flags = 0;  // kAppRow, kAppPage
+  uint32_t off = 0;   // element offset of the row in the caller's rows
+  uint32_t pte = 0;   // entry of the new page
+};
+cp_status decode_impl(cp_pool *p, int32_t n, const int32_t *req_ids, const void *q, void *out, float *lse,
+                      void *hip_stream, const cp_decode_opts *opts, const void *rows,
+                      const std::vector<AppendPlan> *app);
 }  // namespace
 
 struct cp_pool {
@@ -274,6 +284,54 @@ cp_status push_ptes(cp_pool *p, uint64_t lo, uint64_t hi, hipStream_t s) {
   return CP_OK;
 }
 
+
+// Append launches for rows already accounted for in the host tables
+// (old_len[i]: context length before request i's new rows).
+cp_status launch_appends(cp_pool *p, int32_t n, const int32_t *req_ids, const int32_t *n_new, const void *rows,
+                         const uint32_t *old_len, hipStream_t s) {
+  // groups of at most kMaxReqPerLaunch requests and kMaxLaunchModels models.
+  const int32_t P = p->st.page_tokens();
+  uint64_t src = 0;  // element offset of the current request's rows
+  int32_t i = 0;
+  while (i < n) {
+    AppendArgs a{};
+    a.pool = p->dev_pool;
+    a.pte = p->dev_pte;
+    a.rows = (const uint16_t *)rows;
+    int32_t nm = 0, model_map[16];
+    for (int k = 0; k < 16; ++k) model_map[k] = -1;
+    uint32_t grid_rows = 0;
+    while (i < n && a.n_req < kMaxReqPerLaunch) {
+      const Request &r = p->st.req(req_ids[i]);
+      int32_t mi = model_map[r.model];
+      if (mi < 0) {
+        if (nm == kMaxLaunchModels) break;
+        mi = model_map[r.model] = nm;
+        a.geom[nm++] = geom_k(p->st.model(r.model), P);
+      }
+      const Geom &gm = p->st.model(r.model);
+      if (n_new[i] > 0) {
+        AppReq &q = a.req[a.n_req++];
+        q.src_off = src;
+        q.row_begin = grid_rows;
+        q.n_new = (uint32_t)n_new[i];
+        q.old_len = old_len[i];
+        q.pte_base = r.pte_base;
+        q.model = (uint32_t)mi;
+        grid_rows += (uint32_t)n_new[i];
+      }
+      src += (uint64_t)n_new[i] * (uint64_t)gm.row_elems;
+      ++i;
+    }
+    a.total_rows = (int32_t)grid_rows;
+    if (a.n_req > 0) {
+      hipError_t e = launch_append(a, s);
+      if (e != hipSuccess) return hip_fail(e, "append launch");
+    }
+  }
+  return CP_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -323,47 +381,7 @@ cp_status cp_kv_append(cp_pool *p, int32_t n, const int32_t *req_ids, const int3
   rc = push_ptes(p, lo, hi, s);
   if (rc) return rc;
 
-  // Launch groups of at most kMaxReqPerLaunch requests and kMaxLaunchModels models.
-  const int32_t P = p->st.page_tokens();
-  uint64_t src = 0;  // element offset of the current request's rows
-  int32_t i = 0;
-  while (i < n) {
-    AppendArgs a{};
-    a.pool = p->dev_pool;
-    a.pte = p->dev_pte;
-    a.rows = (const uint16_t *)rows;
-    int32_t nm = 0, model_map[16];
-    for (int k = 0; k < 16; ++k) model_map[k] = -1;
-    uint32_t grid_rows = 0;
-    while (i < n && a.n_req < kMaxReqPerLaunch) {
-      const Request &r = p->st.req(req_ids[i]);
-      int32_t mi = model_map[r.model];
-      if (mi < 0) {
-        if (nm == kMaxLaunchModels) break;
-        mi = model_map[r.model] = nm;
-        a.geom[nm++] = geom_k(p->st.model(r.model), P);
-      }
-      const Geom &gm = p->st.model(r.model);
-      if (n_new[i] > 0) {
-        AppReq &q = a.req[a.n_req++];
-        q.src_off = src;
-        q.row_begin = grid_rows;
-        q.n_new = (uint32_t)n_new[i];
-        q.old_len = old_len[i];
-        q.pte_base = r.pte_base;
-        q.model = (uint32_t)mi;
-        grid_rows += (uint32_t)n_new[i];
-      }
-      src += (uint64_t)n_new[i] * (uint64_t)gm.row_elems;
-      ++i;
-    }
-    a.total_rows = (int32_t)grid_rows;
-    if (a.n_req > 0) {
-      hipError_t e = launch_append(a, s);
-      if (e != hipSuccess) return hip_fail(e, "append launch");
-    }
-  }
-  return CP_OK;
+  return launch_appends(p, n, req_ids, n_new, rows, old_len.data(), s);
 }
 
 cp_status cp_kv_gather(cp_pool *p, int32_t req_id, int64_t start, int64_t n_tok, void *dst, void *hip_stream) {
@@ -480,6 +498,17 @@ extern "C" {
 
 cp_status cp_attn_decode_ex(cp_pool *p, int32_t n, const int32_t *req_ids, const void *q, void *out, float *lse,
                             void *hip_stream, const cp_decode_opts *opts) {
+  return decode_impl(p, n, req_ids, q, out, lse, hip_stream, opts, nullptr, nullptr);
+}
+
+}  // extern "C"
+
+namespace {
+
+// Checks what every decode call needs; fills the options and the per-model
+// kernel geometry (variant, head blocking, page cost).
+cp_status decode_prepare(cp_pool *p, int32_t n, const int32_t *req_ids, const void *q, void *out, float *lse,
+                         const cp_decode_opts *opts, cp_decode_opts *o_out, std::vector<GeomK> *gk_out) {
   if (!p) return fail(CP_EINVAL, "null pool");
   if (p->host_only) return fail(CP_ESTATE, "host-only pool cannot decode");
   if (n < 1) return fail(CP_EINVAL, "decode needs at least one request");
@@ -495,10 +524,6 @@ cp_status cp_attn_decode_ex(cp_pool *p, int32_t n, const int32_t *req_ids, const
   if (o.schedule == CP_SCHED_BALANCED && o.num_splits != 0)
     return fail(CP_EINVAL, "num_splits applies to the queue and grid schedules only");
   const int32_t P = p->st.page_tokens();
-  for (int32_t i = 0; i < n; ++i) {
-    const Request &r = p->st.req(req_ids[i]);
-    if (r.ctx_len < 1) return fail(CP_EINVAL, "request %d has an empty context", req_ids[i]);
-  }
 
   // Per-model kernel variant, head blocking and page cost.
   std::vector<GeomK> gk(p->st.n_models());
@@ -521,6 +546,25 @@ cp_status cp_attn_decode_ex(cp_pool *p, int32_t n, const int32_t *req_ids, const
     const int32_t m = p->st.req(req_ids[i]).model;
     if (o.path == CP_PATH_MFMA && gk[m].variant < kMatrixFirst)
       return fail(CP_EINVAL, "model %d has no matrix-core variant (needs a group of 8, 16, 32, 64 or 128 query heads per KV head)", m);
+  }
+  *o_out = o;
+  *gk_out = std::move(gk);
+  return CP_OK;
+}
+
+// The decode of cp_attn_decode_ex; with `app` (one entry per request, call
+// order) the launches also perform the fused appends of cp_attn_decode_step.
+cp_status decode_impl(cp_pool *p, int32_t n, const int32_t *req_ids, const void *q, void *out, float *lse,
+                      void *hip_stream, const cp_decode_opts *opts, const void *rows,
+                      const std::vector<AppendPlan> *app) {
+  cp_decode_opts o{};
+  std::vector<GeomK> gk;
+  cp_status rc = decode_prepare(p, n, req_ids, q, out, lse, opts, &o, &gk);
+  if (rc) return rc;
+  const int32_t P = p->st.page_tokens();
+  for (int32_t i = 0; i < n; ++i) {
+    const Request &r = p->st.req(req_ids[i]);
+    if (r.ctx_len < 1) return fail(CP_EINVAL, "request %d has an empty context", req_ids[i]);
   }
 
   // Packed offsets in call order.
@@ -685,6 +729,7 @@ cp_status cp_attn_decode_ex(cp_pool *p, int32_t n, const int32_t *req_ids, const
     a.q = (const uint16_t *)q;
     a.out = (uint16_t *)out;
     a.lse = lse;
+    a.rows = (const uint16_t *)rows;
     a.ws_o = p->ws_o;
     a.ws_l = p->ws_l;
     a.queue = p->queue;
@@ -707,6 +752,11 @@ cp_status cp_attn_decode_ex(cp_pool *p, int32_t n, const int32_t *req_ids, const
       d.n_chunks = (uint16_t)n_slots[i];
       d.model = (uint8_t)(std::find(g.models.begin(), g.models.end(), r.model) - g.models.begin());
       d.n_hblk = (uint16_t)hblk[i];
+      if (app) {
+        d.app_flags = (*app)[i].flags;
+        d.app_off = (*app)[i].off;
+        d.app_pte = (*app)[i].pte;
+      }
     }
     if (g.grid > 0xFFFF && o.schedule == CP_SCHED_BALANCED) return fail(CP_EINVAL, "too many workers");
     const int v0 = __builtin_ctz(g.mask);
@@ -753,9 +803,71 @@ cp_status cp_attn_decode_ex(cp_pool *p, int32_t n, const int32_t *req_ids, const
   return flush();
 }
 
+}  // namespace
+
+extern "C" {
+
 cp_status cp_attn_decode(cp_pool *p, int32_t n, const int32_t *req_ids, const void *q, void *out, float *lse,
                          void *hip_stream) {
   return cp_attn_decode_ex(p, n, req_ids, q, out, lse, hip_stream, nullptr);
+}
+
+cp_status cp_attn_decode_step(cp_pool *p, int32_t n, const int32_t *req_ids, const int32_t *n_new, const void *rows,
+                              const void *q, void *out, float *lse, void *hip_stream, const cp_decode_opts *opts) {
+  cp_decode_opts o{};
+  std::vector<GeomK> gk;
+  cp_status rc = decode_prepare(p, n, req_ids, q, out, lse, opts, &o, &gk);
+  if (rc) return rc;
+  if (!n_new) return fail(CP_EINVAL, "null n_new");
+  bool any = false;
+  for (int32_t i = 0; i < n; ++i) {
+    if (n_new[i] != 0 && n_new[i] != 1)
+      return fail(CP_EINVAL, "cp_attn_decode_step appends 0 or 1 rows per request (request %d: %d)", req_ids[i],
+                  n_new[i]);
+    const Request &r = p->st.req(req_ids[i]);
+    if (r.ctx_len + n_new[i] < 1) return fail(CP_EINVAL, "request %d has an empty context", req_ids[i]);
+    if (r.ctx_len + n_new[i] > 0xFFFFFFF0ll) return fail(CP_EINVAL, "context length overflow");
+    if (!p->st.fits_reservation(req_ids[i], r.ctx_len + n_new[i]))
+      return fail(CP_EINVAL, "request %d would grow past its reservation of %lld pages", req_ids[i],
+                  (long long)r.reserve_pages);
+    any = any || n_new[i] != 0;
+  }
+  if (any && !rows) return fail(CP_EINVAL, "null rows");
+  if (!any) return cp_attn_decode_ex(p, n, req_ids, q, out, lse, hip_stream, opts);
+
+  // Allocate the new pages on the host; their entries travel with the launch.
+  std::vector<AppendPlan> plan(n);
+  uint64_t off = 0, lo = UINT64_MAX, hi = 0;
+  for (int32_t i = 0; i < n; ++i) {
+    if (!n_new[i]) continue;
+    const Request &r = p->st.req(req_ids[i]);
+    const int32_t row_elems = p->st.model(r.model).row_elems;
+    uint64_t first, count;
+    p->st.grow(req_ids[i], r.ctx_len + 1, &first, &count);
+    plan[i].flags = kAppRow;
+    plan[i].off = (uint32_t)off;
+    if (count) {
+      plan[i].flags |= kAppPage;
+      plan[i].pte = p->st.pte_mirror()[first];
+      lo = std::min(lo, first);
+      hi = std::max(hi, first + count);
+    }
+    off += (uint64_t)row_elems;
+    if (off > 0xFFFFFFFFull) return fail(CP_EINVAL, "too many rows in one call");
+  }
+  rc = decode_impl(p, n, req_ids, q, out, lse, hip_stream, &o, rows, &plan);
+  if (rc) {
+    // keep the device pool in step with the host tables: write the new page
+    // entries and rows the unfused way (rewriting a fused row is harmless)
+    const std::string msg = cp_last_error();
+    DeviceGuard g(p->device);
+    std::vector<uint32_t> old_len(n);
+    for (int32_t i = 0; i < n; ++i) old_len[i] = (uint32_t)(p->st.req(req_ids[i]).ctx_len - n_new[i]);
+    push_ptes(p, lo, hi, (hipStream_t)hip_stream);
+    launch_appends(p, n, req_ids, n_new, rows, old_len.data(), (hipStream_t)hip_stream);
+    return fail(rc, "%s", msg.c_str());
+  }
+  return CP_OK;
 }
 
 }  // extern "C"

@@ -68,13 +68,18 @@ struct DecReq {
   uint16_t chunk_pages;  // queue/grid: pages per KV range; balanced: first worker of the request
   uint16_t n_chunks;     // KV ranges = partial slots
   uint8_t model;         // index into DecodeArgs::geom
-  uint8_t pad;
+  uint8_t app_flags;     // fused append: kAppRow (the last context token is a new row at
+                         // DecodeArgs::rows + app_off), kAppPage (its page is new: app_pte)
   uint16_t n_hblk;       // head blocks per KV range
+  uint32_t app_off;      // element offset of the new row in DecodeArgs::rows
+  uint32_t app_pte;      // page-table entry of the new row's page when kAppPage is set
 };
+enum : uint8_t { kAppRow = 1, kAppPage = 2 };
 
 struct DecodeArgs {
-  const uint8_t *pool;
-  const uint32_t *pte;
+  uint8_t *pool;          // written only by the fused append
+  uint32_t *pte;          // written only by the fused append (a new page's entry)
+  const uint16_t *rows;   // fused append: new logical rows, packed in call order
   const uint16_t *q;
   uint16_t *out;
   float *lse;
@@ -131,7 +136,7 @@ struct GatherArgs {
 };
 
 static_assert(kMaxReqPerLaunch <= 64, "request lookups search one key per lane");
-static_assert(sizeof(DecodeArgs) <= 3072, "decode kernel arguments too large");
+static_assert(sizeof(DecodeArgs) <= 3584, "decode kernel arguments too large");
 static_assert(sizeof(MergeArgs) <= 3072, "merge kernel arguments too large");
 static_assert(sizeof(AppendArgs) <= 3072, "append kernel arguments too large");
 

@@ -52,6 +52,33 @@ __device__ __forceinline__ int unit_segment(const DecodeArgs &a, uint32_t u, Seg
   return r;
 }
 
+// Fused append (cp_attn_decode_step): every piece whose page range holds a
+// request's last context token, when that token is new in this call, first
+// writes the page-table entry of a newly allocated page and copies the new
+// logical row into its page; then the piece reads the page as usual. When
+// several pieces (head blocks) cover that page they all write the same
+// bytes, which is harmless; each one's own stores precede its loads through
+// the workgroup barrier.
+__device__ __forceinline__ void fused_append(const DecodeArgs &a, const DecReq &rq, const Seg &sg) {
+  const GeomK &g = a.geom[rq.model];
+  const uint32_t P = (uint32_t)g.page_tokens;
+  const uint32_t pos = rq.ctx_len - 1, pg = pos / P;
+  if (pg < sg.pg_begin || pg >= sg.pg_end) return;
+  uint32_t pte;
+  if (rq.app_flags & kAppPage) {
+    pte = rq.app_pte;
+    if (threadIdx.x == 0) a.pte[rq.pte_base + pg] = pte;
+  } else {
+    pte = a.pte[rq.pte_base + pg];
+  }
+  uint8_t *page = a.pool + ((uint64_t)pte << 8);
+  const uint4 *src = reinterpret_cast<const uint4 *>(a.rows + rq.app_off);
+  const uint32_t nseg = (uint32_t)g.row_elems / 8;
+  for (uint32_t sgi = threadIdx.x; sgi < nseg; sgi += blockDim.x)
+    *reinterpret_cast<uint4 *>(page + row_seg_offset(g, pos % P, sgi)) = src[sgi];
+  __syncthreads();
+}
+
 // Work loop of every decode kernel; `seg` is inlined once. Queue schedule:
 // workgroups pull unit indices from a device counter until the queue is
 // empty; the last workgroup to leave resets the counters for the next
@@ -85,6 +112,7 @@ __device__ __forceinline__ void decode_loop(const DecodeArgs &a, uint32_t *next,
       r = unit_segment(a, u, &sg);
     }
     first = false;
+    if (a.req[r].app_flags & kAppRow) fused_append(a, a.req[r], sg);
     seg(a.req[r], sg);
     __syncthreads();  // LDS reuse by the next piece
   }
