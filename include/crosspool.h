@@ -292,6 +292,51 @@ cp_status cp_attn_decode_step(cp_pool *pool, int32_t n, const int32_t *req_ids, 
  * pool), CP_EHIP. */
 cp_status cp_kv_gather(cp_pool *pool, int32_t req_id, int64_t start, int64_t n_tok, void *dst, void *hip_stream);
 
+/* ---------------------------------------------------------------------
+ * KV-cache planner (Section 3.1, "KV-cache Planner and Virtualizer",
+ * Eq. 1-2): the pool budget for cp_pool_desc.pool_bytes, host only.
+ *
+ * Request i of a model arrives at A_i with prompt tokens O_p,i, output
+ * tokens O_d,i and decode residence time T_i; its active KV at age u is
+ * kappa * (O_p,i + O_d,i * u / T_i) for 0 <= u < T_i and 0 otherwise
+ * (Eq. 1); the pool demand at time t is the sum over the requests of every
+ * model (Eq. 2). The planner draws Poisson arrivals of rate arrival_rate per
+ * model over [0, horizon_s), each taking one whole trace record (keeping the
+ * correlations between the three quantities), evaluates the demand at n_obs
+ * observation times uniform over [W, horizon_s) (W: the longest residence
+ * time in any trace), and takes the quantile as the order statistic of rank
+ * ceil(quantile * n_obs). The budget is that quantile rounded up to whole
+ * chunk_bytes units. Random draws: SplitMix64 (Steele, Lea and Flood, 2014)
+ * seeded with `seed`, in the order inter-arrival uniform, record uniform per
+ * arrival, model by model, then the observation uniforms.
+ * ------------------------------------------------------------------- */
+typedef struct {
+  double         kappa_bytes;     /* kappa(M): KV bytes per token, > 0 */
+  double         arrival_rate;    /* lambda_M: requests per second, > 0 */
+  int64_t        n_samples;       /* trace records, >= 1 */
+  const int64_t *prompt_tokens;   /* host, n_samples entries, >= 0 */
+  const int64_t *output_tokens;   /* host, n_samples entries, >= 0 */
+  const double  *service_time_s;  /* host, n_samples entries: residence time T, > 0 */
+} cp_plan_model;
+typedef struct {
+  double   horizon_s;    /* simulated window; must exceed every residence time */
+  int64_t  n_obs;        /* observation times, >= 1 */
+  double   quantile;     /* provisioning quantile in (0, 1], e.g. 0.95 or 0.99 */
+  uint64_t seed;
+  uint64_t chunk_bytes;  /* rounding unit of the budget (the pool's allocator chunk) */
+} cp_plan_opts;
+typedef struct {
+  double   quantile_bytes;  /* the demand quantile */
+  double   mean_bytes;      /* mean demand over the observations */
+  double   max_bytes;       /* largest observed demand */
+  uint64_t pool_bytes;      /* quantile_bytes rounded up to whole chunk_bytes */
+  int64_t  n_arrivals;      /* simulated requests */
+} cp_plan_result;
+/* models: host array of n_models descriptors (not retained). Errors:
+ * CP_EINVAL (empty or non-positive inputs, horizon not past the longest
+ * residence time, more than 1e8 expected arrivals for a model). */
+cp_status cp_plan_pool(const cp_plan_model *models, int32_t n_models, const cp_plan_opts *opts, cp_plan_result *out);
+
 #ifdef __cplusplus
 }
 #endif

@@ -14,3 +14,4 @@ from .attention import (  # noqa: F401
     mla_absorb_query,
     mla_explicit,
 )
+from . import planner  # noqa: F401,E402

@@ -24,7 +24,7 @@ DEVICE_FLAGS = ["--offload-arch=gfx950", "-Xclang", "-target-feature", "-Xclang"
 KERNEL_FLAGS = ["-mllvm", "-amdgpu-mfma-vgpr-form"]
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-function", f"-I{os.path.join(ROOT, 'include')}", f"-I{CSRC}"]
 
-SOURCES = ["api.cpp", "pool.cpp", "kernels.hip", "wide_kernels.hip"]
+SOURCES = ["api.cpp", "pool.cpp", "planner.cpp", "kernels.hip", "wide_kernels.hip"]
 
 
 def _run(cmd):

@@ -90,6 +90,22 @@ class cp_decode_opts(C.Structure):
     ]
 
 
+class cp_plan_model(C.Structure):
+    _fields_ = [("kappa_bytes", C.c_double), ("arrival_rate", C.c_double), ("n_samples", C.c_int64),
+                ("prompt_tokens", C.POINTER(C.c_int64)), ("output_tokens", C.POINTER(C.c_int64)),
+                ("service_time_s", C.POINTER(C.c_double))]
+
+
+class cp_plan_opts(C.Structure):
+    _fields_ = [("horizon_s", C.c_double), ("n_obs", C.c_int64), ("quantile", C.c_double), ("seed", C.c_uint64),
+                ("chunk_bytes", C.c_uint64)]
+
+
+class cp_plan_result(C.Structure):
+    _fields_ = [("quantile_bytes", C.c_double), ("mean_bytes", C.c_double), ("max_bytes", C.c_double),
+                ("pool_bytes", C.c_uint64), ("n_arrivals", C.c_int64)]
+
+
 def _load() -> C.CDLL:
     # PyTorch ships its own HIP runtime (soname libamdhip64.so.7, like the
     # system one). Loading torch first makes the library bind to that same
@@ -120,6 +136,7 @@ def _load() -> C.CDLL:
         "cp_attn_decode_step": ([P, I32, C.POINTER(I32), C.POINTER(I32), VP, VP, VP, VP, VP, C.POINTER(cp_decode_opts)],
                                 I32),
         "cp_kv_gather": ([P, I32, I64, I64, VP, VP], I32),
+        "cp_plan_pool": ([C.POINTER(cp_plan_model), I32, C.POINTER(cp_plan_opts), C.POINTER(cp_plan_result)], I32),
     }
     for name, (args, res) in sig.items():
         fn = getattr(lib, name)
@@ -266,6 +283,26 @@ def cp_attn_decode_step(pool: int, req_ids: Sequence[int], n_new: Sequence[int],
 
 def cp_kv_gather(pool: int, req_id: int, start: int, n_tok: int, dst, stream=None) -> None:
     _check(LIB.cp_kv_gather(pool, req_id, start, n_tok, _ptr(dst), _stream(stream)))
+
+
+def cp_plan_pool(models, horizon_s: float, n_obs: int, quantile: float, seed: int, chunk_bytes: int = 2 << 20) -> dict:
+    """models: sequence of dicts with kappa_bytes, arrival_rate and equal-length
+    prompt_tokens / output_tokens / service_time_s sequences (trace records)."""
+    keep = []
+    arr = (cp_plan_model * len(models))()
+    for i, m in enumerate(models):
+        op = (C.c_int64 * len(m["prompt_tokens"]))(*[int(x) for x in m["prompt_tokens"]])
+        od = (C.c_int64 * len(m["output_tokens"]))(*[int(x) for x in m["output_tokens"]])
+        tr = (C.c_double * len(m["service_time_s"]))(*[float(x) for x in m["service_time_s"]])
+        if not (len(op) == len(od) == len(tr)):
+            raise ValueError("trace columns differ in length")
+        keep += [op, od, tr]
+        arr[i] = cp_plan_model(float(m["kappa_bytes"]), float(m["arrival_rate"]), len(op), op, od, tr)
+    o = cp_plan_opts(float(horizon_s), int(n_obs), float(quantile), int(seed) & ((1 << 64) - 1), int(chunk_bytes))
+    r = cp_plan_result()
+    _check(LIB.cp_plan_pool(arr, len(models), C.byref(o), C.byref(r)))
+    return dict(quantile_bytes=r.quantile_bytes, mean_bytes=r.mean_bytes, max_bytes=r.max_bytes,
+                pool_bytes=r.pool_bytes, n_arrivals=r.n_arrivals)
 
 
 # -------------------------------------------------------- convenience ----

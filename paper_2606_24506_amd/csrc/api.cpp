@@ -12,6 +12,7 @@
 
 #include "crosspool.h"
 #include "kargs.h"
+#include "status.hpp"
 #include "pool.hpp"
 
 namespace cp {
@@ -29,9 +30,10 @@ hipError_t launch_merge(const MergeArgs &a, hipStream_t stream);
 using namespace cp;
 
 namespace {
-
 thread_local std::string g_err;
+}  // namespace
 
+namespace cp {
 cp_status fail(cp_status code, const char *fmt, ...) {
   char buf[512];
   va_list ap;
@@ -41,6 +43,9 @@ cp_status fail(cp_status code, const char *fmt, ...) {
   g_err = buf;
   return code;
 }
+}  // namespace cp
+
+namespace {
 
 cp_status hip_fail(hipError_t e, const char *what) {
   return fail(CP_EHIP, "%s: %s", what, hipGetErrorString(e));
