@@ -8,6 +8,7 @@
 #include <cstdio>
 #include <cstring>
 #include <string>
+#include <type_traits>
 #include <vector>
 
 #include "crosspool.h"
@@ -87,10 +88,10 @@ struct cp_pool {
   uint32_t *dev_pte = nullptr;
   uint32_t *pin_pte = nullptr;  // pinned staging copy of the page table
   uint32_t *queue = nullptr;    // work-queue counters
-  float *ws_o = nullptr;
+  uint16_t *ws_o = nullptr;  // split partial outputs (bf16)
   float *ws_l = nullptr;
-  uint64_t ws_o_cap = 0, ws_l_cap = 0;  // floats
-  std::vector<float *> ws_retired;        // outgrown workspaces, freed with the pool
+  uint64_t ws_o_cap = 0, ws_l_cap = 0;  // elements
+  std::vector<void *> ws_retired;         // outgrown workspaces, freed with the pool
   int num_cus = 256;
 };
 
@@ -165,7 +166,7 @@ cp_status cp_pool_destroy(cp_pool *p) {
     if (p->queue) (void)hipFree(p->queue);
     if (p->ws_o) (void)hipFree(p->ws_o);
     if (p->ws_l) (void)hipFree(p->ws_l);
-    for (float *w : p->ws_retired) (void)hipFree(w);
+    for (void *w : p->ws_retired) (void)hipFree(w);
   }
   delete p;
   return CP_OK;
@@ -476,23 +477,25 @@ int32_t units_per_range(const Geom &g, const GeomK &k) {
   return g.hkv * k.nb;
 }
 
-cp_status ensure_ws(cp_pool *p, uint64_t o_floats, uint64_t l_floats) {
-  if (o_floats <= p->ws_o_cap && l_floats <= p->ws_l_cap) return CP_OK;
+// Split workspace: o_elems bf16 partial outputs and l_floats fp32 partial
+// lse values.
+cp_status ensure_ws(cp_pool *p, uint64_t o_elems, uint64_t l_floats) {
+  if (o_elems <= p->ws_o_cap && l_floats <= p->ws_l_cap) return CP_OK;
   // Growth allocates twice what is asked, so that the slow drift of split
   // plans as contexts grow rarely repeats it, and keeps the old buffers
   // until the pool is destroyed: kernels already queued may still use them,
   // and freeing them here would stall the host until the device drains.
-  auto grow = [&](float **buf, uint64_t *cap, uint64_t need) -> cp_status {
+  auto grow = [&](auto **buf, uint64_t *cap, uint64_t need) -> cp_status {
     if (need <= *cap) return CP_OK;
     const uint64_t c = std::max<uint64_t>(2 * need, 2 * *cap);
-    float *nb = nullptr;
-    if (hipMalloc((void **)&nb, c * 4) != hipSuccess) return fail(CP_ENOMEM, "workspace allocation failed");
+    void *nb = nullptr;
+    if (hipMalloc(&nb, c * sizeof(**buf)) != hipSuccess) return fail(CP_ENOMEM, "workspace allocation failed");
     if (*buf) p->ws_retired.push_back(*buf);
-    *buf = nb;
+    *buf = static_cast<std::remove_reference_t<decltype(*buf)>>(nb);
     *cap = c;
     return CP_OK;
   };
-  cp_status rc = grow(&p->ws_o, &p->ws_o_cap, o_floats);
+  cp_status rc = grow(&p->ws_o, &p->ws_o_cap, o_elems);
   if (rc) return rc;
   return grow(&p->ws_l, &p->ws_l_cap, l_floats);
 }
@@ -704,23 +707,23 @@ cp_status decode_impl(cp_pool *p, int32_t n, const int32_t *req_ids, const void 
   }
 
   // Workspace for requests split over several slots.
-  uint64_t ws_rows = 0, ws_floats = 0;
+  uint64_t ws_rows = 0, ws_elems = 0;
   std::vector<uint32_t> ws_base(n, kNoWs), ws_orow(n, 0);
   for (int32_t i = 0; i < n; ++i) {
     if (n_slots[i] <= 1) continue;
     const Geom &g = p->st.model(model_of(i));
     ws_base[i] = (uint32_t)ws_rows;
     ws_rows += (uint64_t)n_slots[i] * g.hq;
-    ws_floats = (ws_floats + 511) / 512 * 512;
-    ws_orow[i] = (uint32_t)(ws_floats / (uint64_t)g.d_v);
-    ws_floats += (uint64_t)n_slots[i] * g.hq * g.d_v;
+    ws_elems = (ws_elems + 511) / 512 * 512;
+    ws_orow[i] = (uint32_t)(ws_elems / (uint64_t)g.d_v);
+    ws_elems += (uint64_t)n_slots[i] * g.hq * g.d_v;
   }
-  if (ws_rows >= kNoWs || ws_floats / 64 >= kNoWs) return fail(CP_EINVAL, "split workspace too large");
+  if (ws_rows >= kNoWs || ws_elems / 64 >= kNoWs) return fail(CP_EINVAL, "split workspace too large");
 
   DeviceGuard dg(p->device);
   hipStream_t s = (hipStream_t)hip_stream;
   if (ws_rows) {
-    rc = ensure_ws(p, ws_floats, ws_rows);
+    rc = ensure_ws(p, ws_elems, ws_rows);
     if (rc) return rc;
   }
   // The caller's events take the start of the first decode launch and the

@@ -391,14 +391,9 @@ __device__ __forceinline__ void mla_unit(const DecodeArgs &a, const GeomK &gm, c
     for (int db = 0; db < C::DBW; ++db) {
       const int d = (C::DV / NW) * wave + 16 * db + 4 * quad;
       const f32x4 v = o[db][hb] * inv;
-      if (split) {
-        *reinterpret_cast<f32x4 *>(a.ws_o + ((uint64_t)rq.ws_orow + (uint64_t)slot * gm.hq + head) * C::DV + d) = v;
-      } else {
-        uint2 pk;
-        pk.x = f32_to_bf16(v[0]) | (f32_to_bf16(v[1]) << 16);
-        pk.y = f32_to_bf16(v[2]) | (f32_to_bf16(v[3]) << 16);
-        *reinterpret_cast<uint2 *>(a.out + rq.o_off + head * C::DV + d) = pk;
-      }
+      uint16_t *dst = split ? a.ws_o + ((uint64_t)rq.ws_orow + (uint64_t)slot * gm.hq + head) * C::DV + d
+                            : a.out + rq.o_off + head * C::DV + d;
+      *reinterpret_cast<uint2 *>(dst) = bf16x4_bits(v[0], v[1], v[2], v[3]);
     }
   }
   if (quad == 0) {

@@ -388,14 +388,9 @@ __device__ __forceinline__ void narrow_unit(const DecodeArgs &a, const GeomK &gm
   const bool split = rq.ws_base != kNoWs;
   auto write_out = [&](int hh, int d, const f32x4 &v) {  // hh: head within the unit
     const uint32_t head = (uint32_t)(h0 + hh);
-    if (split) {
-      *reinterpret_cast<f32x4 *>(a.ws_o + ((uint64_t)rq.ws_orow + (uint64_t)slot * gm.hq + head) * DV + d) = v;
-    } else {
-      uint2 pk;
-      pk.x = f32_to_bf16(v[0]) | (f32_to_bf16(v[1]) << 16);
-      pk.y = f32_to_bf16(v[2]) | (f32_to_bf16(v[3]) << 16);
-      *reinterpret_cast<uint2 *>(a.out + rq.o_off + head * DV + d) = pk;
-    }
+    uint16_t *dst = split ? a.ws_o + ((uint64_t)rq.ws_orow + (uint64_t)slot * gm.hq + head) * DV + d
+                          : a.out + rq.o_off + head * DV + d;
+    *reinterpret_cast<uint2 *>(dst) = bf16x4_bits(v[0], v[1], v[2], v[3]);
   };
   auto write_lse = [&](int hh, float lse) {
     const uint32_t head = (uint32_t)(h0 + hh);

@@ -250,13 +250,11 @@ __device__ __forceinline__ void small_unit(const DecodeArgs &a, const GeomK &gm,
     if (h < hv) {
       const uint32_t head = (uint32_t)(h0 + h);
       const f32x4 x = v * (1.0f / L);
+      const uint2 pk = bf16x4_bits(x[0], x[1], x[2], x[3]);
       if (split) {
-        *reinterpret_cast<f32x4 *>(a.ws_o + ((uint64_t)rq.ws_orow + (uint64_t)slot * gm.hq + head) * D + d) = x;
+        *reinterpret_cast<uint2 *>(a.ws_o + ((uint64_t)rq.ws_orow + (uint64_t)slot * gm.hq + head) * D + d) = pk;
         if (d == 0) a.ws_l[(uint64_t)rq.ws_base + (uint64_t)slot * gm.hq + head] = (M + fast_log2(L)) * kLn2;
       } else {
-        uint2 pk;
-        pk.x = f32_to_bf16(x[0]) | (f32_to_bf16(x[1]) << 16);
-        pk.y = f32_to_bf16(x[2]) | (f32_to_bf16(x[3]) << 16);
         *reinterpret_cast<uint2 *>(a.out + rq.o_off + head * D + d) = pk;
         if (d == 0) a.lse[rq.lse_off + head] = (M + fast_log2(L)) * kLn2;
       }

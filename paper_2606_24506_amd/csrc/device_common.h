@@ -55,6 +55,14 @@ CP_DEV const uint8_t *page_ptr(const uint8_t *pool, const uint32_t *pte, uint32_
 
 // Byte offset, inside a page, of 16-byte segment `seg` of the logical row of
 // token slot `slot` (row = [K heads | V heads] for GQA, [latent | rope] for MLA).
+// Four floats rounded to bf16 (nearest even), packed in element order.
+CP_DEV uint2 bf16x4_bits(float x0, float x1, float x2, float x3) {
+  uint2 pk;
+  pk.x = f32_to_bf16(x0) | (f32_to_bf16(x1) << 16);
+  pk.y = f32_to_bf16(x2) | (f32_to_bf16(x3) << 16);
+  return pk;
+}
+
 CP_DEV uint64_t row_seg_offset(const GeomK &g, uint32_t slot, uint32_t seg) {
   const uint32_t e = seg * 8;  // first bf16 element of the segment
   if (g.kind == 0) return (uint64_t)slot * (uint32_t)(g.d_k * 2) + (uint64_t)e * 2;

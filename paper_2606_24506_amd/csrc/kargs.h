@@ -63,7 +63,7 @@ struct DecReq {
   uint32_t o_off;     // bf16 element offset of its outputs
   uint32_t lse_off;   // float offset of its log-sum-exp values
   uint32_t ws_base;   // first partial lse row (kNoWs when the request is not split)
-  uint32_t ws_orow;   // partial outputs start at float offset ws_orow * d_v
+  uint32_t ws_orow;   // partial outputs start at element offset ws_orow * d_v
   uint32_t unit_begin;   // queue/grid: first unit; balanced: cost prefix of the request
   uint16_t chunk_pages;  // queue/grid: pages per KV range; balanced: first worker of the request
   uint16_t n_chunks;     // KV ranges = partial slots
@@ -83,7 +83,7 @@ struct DecodeArgs {
   const uint16_t *q;
   uint16_t *out;
   float *lse;
-  float *ws_o;        // partial outputs, [row][d_v] fp32, normalised
+  uint16_t *ws_o;     // partial outputs, [row][d_v] bf16, normalised
   float *ws_l;        // partial log-sum-exp, [row], natural log
   uint32_t *queue;    // queue schedule: {next unit, finished workgroups}
   int32_t n_req, n_units;
@@ -100,7 +100,7 @@ struct MergeReq {
 };
 
 struct MergeArgs {
-  const float *ws_o;
+  const uint16_t *ws_o;
   const float *ws_l;
   uint16_t *out;
   float *lse;

@@ -234,7 +234,7 @@ __device__ __forceinline__ void valu_unit(const DecodeArgs &a, const GeomK &gm, 
     const float o = acc_s[h * dv + d] / Lh;
     const uint32_t qh = (uint32_t)(h0 + h);
     if (split)
-      a.ws_o[((uint64_t)rq.ws_orow + (uint64_t)chunk * gm.hq + qh) * dv + d] = o;
+      a.ws_o[((uint64_t)rq.ws_orow + (uint64_t)chunk * gm.hq + qh) * dv + d] = (uint16_t)f32_to_bf16(o);
     else
       a.out[rq.o_off + qh * dv + d] = (uint16_t)f32_to_bf16(o);
   }
@@ -456,7 +456,7 @@ __global__ __launch_bounds__(256) void merge_kernel(const MergeArgs a) {
   const uint32_t per = dv >= 128 ? 2 : dv / 64;  // floats per lane
   const uint32_t d0 = db * 128 + lane * per;
   float acc0 = 0.f, acc1 = 0.f, l = 0.f;
-  const float *obase = a.ws_o + ((uint64_t)rq.ws_orow + h) * dv + d0;
+  const uint16_t *obase = a.ws_o + ((uint64_t)rq.ws_orow + h) * dv + d0;
   const uint64_t ostride = (uint64_t)rq.hq * dv;
   uint32_t c = wave;
   for (; c + 12 < n; c += 16) {
@@ -465,9 +465,9 @@ __global__ __launch_bounds__(256) void merge_kernel(const MergeArgs a) {
     for (int u = 0; u < 4; ++u) {
       const uint32_t cc = c + 4 * u;
       w[u] = a.ws_l[lrow0 + (uint64_t)cc * rq.hq];
-      const float *src = obase + (uint64_t)cc * ostride;
-      x0[u] = src[0];
-      x1[u] = per > 1 ? src[1] : 0.f;
+      const uint16_t *src = obase + (uint64_t)cc * ostride;
+      x0[u] = bf16_to_f32(src[0]);
+      x1[u] = per > 1 ? bf16_to_f32(src[1]) : 0.f;
     }
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
@@ -479,10 +479,10 @@ __global__ __launch_bounds__(256) void merge_kernel(const MergeArgs a) {
   }
   for (; c < n; c += 4) {
     const float wu = fast_exp2(a.ws_l[lrow0 + (uint64_t)c * rq.hq] * kLog2e - M);
-    const float *src = obase + (uint64_t)c * ostride;
+    const uint16_t *src = obase + (uint64_t)c * ostride;
     l += wu;
-    acc0 = fmaf(wu, src[0], acc0);
-    if (per > 1) acc1 = fmaf(wu, src[1], acc1);
+    acc0 = fmaf(wu, bf16_to_f32(src[0]), acc0);
+    if (per > 1) acc1 = fmaf(wu, bf16_to_f32(src[1]), acc1);
   }
   // combine the four waves in order
   if (wave > 0) {
