@@ -28,6 +28,7 @@ import numpy as np
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
+MAX_AUTO_WARMUP = 4000  # cap of the time-based warmup (sets the tokens reserved for growth)
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E
 MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 matrix-core peak
 PROFILE_NAMES = {2: "decode_v2lite_mla16", 3: "decode_v3_mla128", 4: "decode_mixed", 5: "decode_burst_mla128"}
@@ -44,7 +45,10 @@ def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
-    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=-1,
+                    help="untimed warmup steps (default: as many as fill --warmup-seconds of GPU time)")
+    ap.add_argument("--warmup-seconds", type=float, default=0.3,
+                    help="GPU time the default warmup lasts: clocks and power settle within it")
     ap.add_argument("--config", type=int, default=2, choices=[1, 2, 3, 4, 5])
     ap.add_argument("--layers", type=int, default=0, help="KV copies cycled by the steps (0: enough to exceed 1 GiB)")
     ap.add_argument("--path", type=int, default=0, help="0 auto, 1 vector, 2 matrix cores")
@@ -60,12 +64,17 @@ def parse():
 
 
 def kernel_source_hash() -> str:
-    """Hash of the HIP/C++ sources the decode kernel is built from."""
+    """Hash of the sources that decide what a decode launch does: the device
+    code, the host code that plans and launches it, and the page allocator
+    (placement). The pool planner and other host-only sources are left out."""
     import glob
     import hashlib
 
+    csrc = os.path.join(ROOT, "paper_2606_24506_amd", "csrc")
+    files = glob.glob(os.path.join(csrc, "*.hip")) + glob.glob(os.path.join(csrc, "*.h"))
+    files += [os.path.join(csrc, f) for f in ("api.cpp", "pool.cpp", "pool.hpp")]
     h = hashlib.sha256()
-    for fn in sorted(glob.glob(os.path.join(ROOT, "paper_2606_24506_amd", "csrc", "*"))):
+    for fn in sorted(files):
         h.update(os.path.basename(fn).encode())
         h.update(open(fn, "rb").read())
     return h.hexdigest()
@@ -165,7 +174,8 @@ def main():
     wl = make_workload(args.config)
     kv_bytes = sum(rq.ctx_len * wl.model(r).kappa for r, rq in enumerate(wl.requests))
     layers = args.layers or max(1, math.ceil((1 << 30) / kv_bytes))
-    total_steps = args.warmup + 2 * args.steps  # warmup, throughput pass, kernel-timing pass
+    max_warmup = args.warmup if args.warmup >= 0 else MAX_AUTO_WARMUP
+    total_steps = max_warmup + 2 * args.steps  # warmup, throughput pass, kernel-timing pass
     grow = -(-total_steps // layers) + 1
     print(f"[bench] cfg{args.config}: {len(wl.requests)} requests, {kv_bytes / 1e6:.1f} MB KV per layer, "
           f"{layers} layers", file=sys.stderr, flush=True)
@@ -200,33 +210,32 @@ def main():
         else:
             ld.pool.decode_step(ld.req_ids, ones, new_rows, ld.q, ld.out, ld.lse, stream, **opts)
 
-    for i in range(args.warmup):
-        step(i)
-    torch.cuda.synchronize()
-    # algorithmic bytes of the two timed passes (contexts grow by one per visit)
-    ctx0 = [[ld.pool.ctx_len(r) for r in ld.req_ids] for ld in lds]
-    dec_bytes, app_bytes, dec_bytes_timed, dec_flops_timed = 0, 0, 0, 0
-    visits = [0] * layers
-    for i in range(2 * args.steps):
-        li = (args.warmup + i) % layers
-        ctx = [c + visits[li] + 1 for c in ctx0[li]]
-        visits[li] += 1
-        if i < args.steps:
-            dec_bytes += algorithmic_bytes_decode(wl, ctx)
-            app_bytes += sum(2 * wl.model(r).kappa + 4 for r in range(B))
-        else:
-            dec_bytes_timed += algorithmic_bytes_decode(wl, ctx)
-            dec_flops_timed += algorithmic_flops_decode(wl, ctx)
     if args.copy_mib:
         src = torch.empty(args.copy_mib << 20, dtype=torch.uint8, device="cuda")
         dst = torch.empty_like(src)
         dst.copy_(src)
         del src, dst
+    # Warmup. The attention kernels of the 128-head batches draw enough power
+    # that the clocks take tens of milliseconds of continuous work to settle
+    # after an idle gap, so by default the warmup lasts a fixed GPU time: 20
+    # steps measure the step time, then one unbroken run fills the rest.
+    n_warm = args.warmup if args.warmup >= 0 else min(20, MAX_AUTO_WARMUP)
+    t0 = time.perf_counter()
+    for i in range(n_warm):
+        step(i)
     torch.cuda.synchronize()
+    if args.warmup < 0 and n_warm > 0:
+        per_step = (time.perf_counter() - t0) / n_warm
+        more = min(MAX_AUTO_WARMUP, math.ceil(args.warmup_seconds / per_step)) - n_warm
+        for i in range(n_warm, n_warm + max(0, more)):
+            step(i)
+        n_warm += max(0, more)
+        torch.cuda.synchronize()
+    ctx0 = [[ld.pool.ctx_len(r) for r in ld.req_ids] for ld in lds]
     # Throughput pass: K steps with nothing but the work in the stream.
     t0 = time.perf_counter()
     for i in range(args.steps):
-        step(args.warmup + i)
+        step(n_warm + i)
     t_enq = time.perf_counter() - t0
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
@@ -236,9 +245,22 @@ def main():
     # costs the host tens of microseconds per call, enough to leave the GPU
     # waiting, so these steps are not part of the throughput figure.
     for i in range(args.steps):
-        step(args.warmup + args.steps + i, ev[i])
+        step(n_warm + args.steps + i, ev[i])
     torch.cuda.synchronize()
     kern_ms = sum(a.elapsed_time(b) for a, b in ev) / args.steps
+    # algorithmic bytes of the two timed passes (contexts grow by one per visit)
+    dec_bytes, app_bytes, dec_bytes_timed, dec_flops_timed = 0, 0, 0, 0
+    visits = [0] * layers
+    for i in range(2 * args.steps):
+        li = (n_warm + i) % layers
+        ctx = [c + visits[li] + 1 for c in ctx0[li]]
+        visits[li] += 1
+        if i < args.steps:
+            dec_bytes += algorithmic_bytes_decode(wl, ctx)
+            app_bytes += sum(2 * wl.model(r).kappa + 4 for r in range(B))
+        else:
+            dec_bytes_timed += algorithmic_bytes_decode(wl, ctx)
+            dec_flops_timed += algorithmic_flops_decode(wl, ctx)
 
     value = (dec_bytes + app_bytes) / wall / 1e9
     ms_per_step = wall * 1e3 / args.steps
@@ -250,7 +272,7 @@ def main():
         "unit": "GB/s",
         "n_gpus": 1,
         "steps": args.steps,
-        "warmup": args.warmup,
+        "warmup": n_warm,
         "ms_per_step": round(ms_per_step, 5),
         "higher_is_better": True,
         "scaling": "weak",
