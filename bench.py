@@ -56,6 +56,8 @@ def parse():
     ap.add_argument("--schedule", type=int, default=0, help="0 balanced, 1 work queue, 2 one workgroup per unit")
     ap.add_argument("--unfused", action="store_true",
                     help="step as cp_kv_append + cp_attn_decode_ex instead of cp_attn_decode_step")
+    ap.add_argument("--backing", type=int, default=0, choices=[0, 1],
+                    help="pool memory: 0 one device buffer, 1 virtual ranges with chunks mapped on demand")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="target CPU time of the oracle sample")
     ap.add_argument("--copy-mib", type=int, default=0,
@@ -183,7 +185,7 @@ def main():
     rows_cache = {r: wl.rows_bits(r) for r in range(len(wl.requests))}
     inter = 512 if args.config == 4 else (4096 if args.config == 5 else 0)
     lds = [load(wl, reserve_extra=grow, interleave=inter, rows_override=rows_cache,
-                placement_seed=wl.placement_seed + 1000 * i) for i in range(layers)]
+                placement_seed=wl.placement_seed + 1000 * i, backing=args.backing) for i in range(layers)]
     del rows_cache
     B = len(wl.requests)
     # one new token per request per step: seeded rows, resident on the GPU before timing
@@ -289,6 +291,7 @@ def main():
                      else "cp_attn_decode_step: 1 appended token/request + decode, append fused into the launch"),
             "path": ["auto", "vector", "matrix"][args.path],
             "schedule": ["balanced", "queue", "grid"][args.schedule],
+            "backing": ["buffer", "virtual"][args.backing],
         },
         "req_tokens_per_s": round(B / (wall / args.steps), 1),
         "host_enqueue_ms_per_step": round(t_enq * 1e3 / args.steps, 5),

@@ -68,6 +68,28 @@ int32_t cp_version(void);
 
 typedef struct cp_pool cp_pool; /* opaque */
 
+/* Where the pool's pages live (Section 3.1, "KV-cache Planner and
+ * Virtualizer"; Section 4, KV-cache virtualization). */
+typedef enum {
+  /* One device buffer of pool_bytes (allocated, or device_mem), carved
+   * into chunks; all of it is held for the pool's lifetime. */
+  CP_BACKING_BUFFER = 0,
+  /* Virtualized: the pool reserves address space only, one range of
+   * pool_bytes per model (at most 16 models, and at most 1 TiB in all,
+   * which caps the models of budgets above 64 GiB), and maps physical
+   * allocations of chunk_bytes into a model's range on demand: when a
+   * request is admitted, enough chunks to back its whole reservation; at
+   * close, chunks that no open reservation of the model needs any more are
+   * unmapped and their memory returned to the device. Mapping stays on the
+   * admission and release slow paths: appends and decode steps never map.
+   * The budget limits the chunks mapped at once. Kernels see the same
+   * page-table interface as with a buffer. chunk_bytes must be a multiple
+   * of the device's mapping granularity; placement_seed is ignored (the
+   * driver places physical memory); device_mem must be NULL. The mapping
+   * calls wait for the device to finish queued work. */
+  CP_BACKING_VIRTUAL = 1
+} cp_backing;
+
 typedef struct {
   /* Tokens per page, pool-wide (64 in the shipped workloads). A page of a
    * model with kappa bytes per token holds page_tokens * kappa bytes. */
@@ -95,12 +117,14 @@ typedef struct {
   void *device_mem;
   /* Maximum number of simultaneously open requests; 0 means 4096. */
   int32_t max_requests;
-  int32_t reserved0;
+  int32_t backing; /* cp_backing */
 } cp_pool_desc;
 
 /* Create a pool. Errors: CP_EINVAL (page_tokens not in [1, 4096],
- * chunk_bytes not a multiple of 256, fewer than one chunk), CP_ENOMEM
- * (device or pinned-host allocation failed), CP_EHIP. */
+ * chunk_bytes not a multiple of 256, fewer than one chunk, an unknown
+ * backing, a virtual pool on a device without virtual memory management
+ * or with chunk_bytes off its mapping granularity), CP_ENOMEM (device or
+ * pinned-host allocation, or the address reservation, failed), CP_EHIP. */
 cp_status cp_pool_create(const cp_pool_desc *desc, cp_pool **out);
 
 /* Destroy a pool and free what it owns. CP_ESTATE if requests are still
@@ -109,11 +133,15 @@ cp_status cp_pool_destroy(cp_pool *pool);
 
 typedef struct {
   uint64_t chunks_total;   /* whole chunks in the budget */
-  uint64_t chunks_used;    /* chunks currently carved for some model */
+  uint64_t chunks_used;    /* chunks currently carved for some model
+                              (mapped, for a virtual pool) */
   uint64_t pages_used;     /* pages holding KV of open requests */
   uint64_t pages_reserved; /* pages promised to open requests */
   int32_t requests_open;
   int32_t models;
+  uint64_t span_bytes;     /* address range page entries point into */
+  int32_t backing;         /* cp_backing */
+  int32_t max_models;      /* models the pool can register */
 } cp_pool_stats_t;
 
 cp_status cp_pool_stats(cp_pool *pool, cp_pool_stats_t *out);
@@ -164,14 +192,18 @@ cp_status cp_model_info(cp_pool *pool, int32_t model_id, cp_model_info_t *out);
  * budget can hold every open reservation of every model at once, so an
  * admitted request is never refused a page later (Section 3.1: admission
  * queues or rejects new requests rather than interrupting active decodes).
- * Sets *req_id. Errors: CP_ENOSPC (budget exhausted: nothing changed, the
- * caller may queue and retry), CP_EINVAL. */
+ * On a virtual pool the reservation's chunks are mapped here. Sets
+ * *req_id. Errors: CP_ENOSPC (budget exhausted: nothing changed, the
+ * caller may queue and retry), CP_ENOMEM (a virtual pool could not map the
+ * memory: nothing changed), CP_EINVAL. */
 cp_status cp_request_open(cp_pool *pool, int32_t model_id, int64_t reserve_tokens, int32_t *req_id);
 
 /* Release a request: its pages go back to its model's slab, chunks that
  * become empty go back to the shared budget, and its reservation ends
  * (Section 3.1: pages are kept until the request finishes). The caller
- * must have synchronised every stream with work on this request. */
+ * must have synchronised every stream with work on this request. On a
+ * virtual pool, a chunk that empties is unmapped, after one device-wide
+ * synchronisation per call. */
 cp_status cp_request_close(cp_pool *pool, int32_t req_id);
 
 cp_status cp_request_len(cp_pool *pool, int32_t req_id, int64_t *ctx_len);

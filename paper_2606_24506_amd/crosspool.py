@@ -21,6 +21,7 @@ CP_OK, CP_EINVAL, CP_ENOMEM, CP_ENOSPC, CP_EHIP, CP_ESTATE = 0, -1, -2, -3, -4, 
 CP_KIND_MLA, CP_KIND_GQA = 0, 1
 CP_PATH_AUTO, CP_PATH_VALU, CP_PATH_MFMA = 0, 1, 2
 CP_SCHED_BALANCED, CP_SCHED_QUEUE, CP_SCHED_GRID = 0, 1, 2
+CP_BACKING_BUFFER, CP_BACKING_VIRTUAL = 0, 1
 _NAMES = {0: "CP_OK", -1: "CP_EINVAL", -2: "CP_ENOMEM", -3: "CP_ENOSPC", -4: "CP_EHIP", -5: "CP_ESTATE"}
 
 
@@ -40,7 +41,7 @@ class cp_pool_desc(C.Structure):
         ("placement_seed", C.c_uint64),
         ("device_mem", C.c_void_p),
         ("max_requests", C.c_int32),
-        ("reserved0", C.c_int32),
+        ("backing", C.c_int32),
     ]
 
 
@@ -52,6 +53,9 @@ class cp_pool_stats_t(C.Structure):
         ("pages_reserved", C.c_uint64),
         ("requests_open", C.c_int32),
         ("models", C.c_int32),
+        ("span_bytes", C.c_uint64),
+        ("backing", C.c_int32),
+        ("max_models", C.c_int32),
     ]
 
 
@@ -188,8 +192,9 @@ def cp_version() -> int:
 
 
 def cp_pool_create(page_tokens: int = 64, pool_bytes: int = 0, chunk_bytes: int = 0, placement_seed: int = 0,
-                   device: int = 0, device_mem=None, max_requests: int = 0) -> int:
-    d = cp_pool_desc(page_tokens, device, pool_bytes, chunk_bytes, placement_seed, _ptr(device_mem), max_requests, 0)
+                   device: int = 0, device_mem=None, max_requests: int = 0, backing: int = 0) -> int:
+    d = cp_pool_desc(page_tokens, device, pool_bytes, chunk_bytes, placement_seed, _ptr(device_mem), max_requests,
+                     backing)
     out = C.c_void_p()
     _check(LIB.cp_pool_create(C.byref(d), C.byref(out)))
     return out.value

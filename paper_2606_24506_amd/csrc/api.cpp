@@ -9,6 +9,7 @@
 #include <cstring>
 #include <string>
 #include <type_traits>
+#include <unordered_map>
 #include <vector>
 
 #include "crosspool.h"
@@ -83,8 +84,14 @@ struct cp_pool {
   PoolState st;
   int device = -1;
   bool host_only = true;
-  uint8_t *dev_pool = nullptr;
+  uint8_t *dev_pool = nullptr;  // the buffer, or the base of the reserved span
   bool owns_pool = false;
+  // virtual backing: one physical allocation per mapped chunk slot
+  bool vmm = false;
+  bool vmm_synced = false;  // device synchronized since the current close began
+  hipError_t vmm_err = hipSuccess;  // first failed unmap or release of the current close
+  hipMemAllocationProp vmm_prop{};
+  std::unordered_map<int32_t, hipMemGenericAllocationHandle_t> vmm_handles;
   uint32_t *dev_pte = nullptr;
   uint32_t *pin_pte = nullptr;  // pinned staging copy of the page table
   uint32_t *queue = nullptr;    // work-queue counters
@@ -94,6 +101,111 @@ struct cp_pool {
   std::vector<void *> ws_retired;         // outgrown workspaces, freed with the pool
   int num_cus = 256;
 };
+
+namespace {
+
+// Backs chunk slot c of a virtual pool with a fresh physical allocation
+// (Section 4, KV-cache virtualization: pages are mapped on demand, off the
+// per-token path). Returns false, with nothing left mapped, on failure.
+bool vmm_map(cp_pool *p, int32_t c) {
+  DeviceGuard g(p->device);
+  const size_t cb = p->st.chunk_bytes();
+  void *va = p->dev_pool + (uint64_t)c * cb;
+  if (p->vmm_handles.count(c)) return false;  // an earlier unmap of the slot failed
+  hipMemGenericAllocationHandle_t h{};
+  if (hipMemCreate(&h, cb, &p->vmm_prop, 0) != hipSuccess) return false;
+  if (hipMemMap(va, cb, 0, h, 0) != hipSuccess) {
+    (void)hipMemRelease(h);
+    return false;
+  }
+  hipMemAccessDesc ad{};
+  ad.location = p->vmm_prop.location;
+  ad.flags = hipMemAccessFlagsProtReadWrite;
+  if (hipMemSetAccess(va, cb, &ad, 1) != hipSuccess) {
+    (void)hipMemUnmap(va, cb);
+    (void)hipMemRelease(h);
+    return false;
+  }
+  p->vmm_handles[c] = h;
+  return true;
+}
+
+// Releases the physical memory behind chunk slot c. Work still queued on
+// the device may read the slot (a close only requires the caller to have
+// synchronized the closed request's own streams), so the device is drained
+// once per close before the first unmap.
+void vmm_unmap(cp_pool *p, int32_t c) {
+  DeviceGuard g(p->device);
+  if (!p->vmm_synced) {
+    (void)hipDeviceSynchronize();
+    p->vmm_synced = true;
+  }
+  auto it = p->vmm_handles.find(c);
+  if (it == p->vmm_handles.end()) return;
+  const size_t cb = p->st.chunk_bytes();
+  hipError_t e = hipMemUnmap(p->dev_pool + (uint64_t)c * cb, cb);
+  if (e != hipSuccess) {
+    // still mapped: the slot cannot be mapped again (vmm_map refuses it);
+    // destroy retries the unmap
+    if (p->vmm_err == hipSuccess) p->vmm_err = e;
+    return;
+  }
+  e = hipMemRelease(it->second);
+  if (e != hipSuccess && p->vmm_err == hipSuccess) p->vmm_err = e;
+  p->vmm_handles.erase(it);
+}
+
+// Reserves the address span of a virtual pool and installs the mapping
+// hooks of its allocator.
+cp_status vmm_setup(cp_pool *p, int dev) {
+  int supported = 0;
+  if (hipDeviceGetAttribute(&supported, hipDeviceAttributeVirtualMemoryManagementSupported, dev) != hipSuccess ||
+      !supported)
+    return fail(CP_EINVAL, "device %d does not support virtual memory management", dev);
+  p->vmm_prop.type = hipMemAllocationTypePinned;
+  p->vmm_prop.location.type = hipMemLocationTypeDevice;
+  p->vmm_prop.location.id = dev;
+  size_t gran = 0;
+  hipError_t e = hipMemGetAllocationGranularity(&gran, &p->vmm_prop, hipMemAllocationGranularityMinimum);
+  if (e != hipSuccess) return hip_fail(e, "mapping granularity query");
+  const uint64_t cb = p->st.chunk_bytes();
+  if (gran == 0 || cb % gran)
+    return fail(CP_EINVAL, "chunk_bytes (%llu) must be a multiple of the device's mapping granularity (%zu)",
+                (unsigned long long)cb, gran);
+  const size_t align = cb % (2u << 20) == 0 ? (2u << 20) : 0;
+  void *base = nullptr;
+  e = hipMemAddressReserve(&base, p->st.span_bytes(), align, nullptr, 0);
+  if (e != hipSuccess) return fail(CP_ENOMEM, "reserving %llu bytes of address space failed: %s",
+                                   (unsigned long long)p->st.span_bytes(), hipGetErrorString(e));
+  p->dev_pool = (uint8_t *)base;
+  p->vmm = true;
+  p->st.map_chunk = [p](int32_t c) { return vmm_map(p, c); };
+  p->st.unmap_chunk = [p](int32_t c) { vmm_unmap(p, c); };
+  return CP_OK;
+}
+
+// Carves, before any page is allocated, the chunks that growing the
+// requests by n_new tokens needs, so that the allocation itself cannot
+// fail. (A virtual pool mapped these at admission; this then carves
+// nothing.) On failure nothing has changed.
+cp_status prepare_growth(cp_pool *p, int32_t n, const int32_t *ids, const int32_t *n_new) {
+  std::vector<int64_t> need((size_t)p->st.n_models(), 0);
+  for (int32_t i = 0; i < n; ++i) {
+    const Request &r = p->st.req(ids[i]);
+    need[(size_t)r.model] += p->st.pages_to_grow(ids[i], r.ctx_len + n_new[i]);
+  }
+  std::vector<int32_t> carved;
+  for (int32_t m = 0; m < p->st.n_models(); ++m) {
+    if (need[(size_t)m] > 0 && !p->st.ensure_slots(m, need[(size_t)m], &carved)) {
+      p->st.release_empty(carved);
+      return fail(CP_ENOMEM, "could not map physical memory for %lld new pages of model %d",
+                  (long long)need[(size_t)m], m);
+    }
+  }
+  return CP_OK;
+}
+
+}  // namespace
 
 extern "C" {
 
@@ -106,7 +218,17 @@ cp_status cp_pool_create(const cp_pool_desc *d, cp_pool **out) {
   *out = nullptr;
   auto *p = new (std::nothrow) cp_pool();
   if (!p) return fail(CP_ENOMEM, "host allocation failed");
-  std::string e = p->st.init(d->page_tokens, d->pool_bytes, d->chunk_bytes, d->placement_seed, d->max_requests);
+  if (d->backing != CP_BACKING_BUFFER && d->backing != CP_BACKING_VIRTUAL) {
+    delete p;
+    return fail(CP_EINVAL, "unknown backing %d", d->backing);
+  }
+  const bool virt = d->backing == CP_BACKING_VIRTUAL;
+  if (virt && d->device_mem) {
+    delete p;
+    return fail(CP_EINVAL, "a virtual pool maps its own memory: device_mem must be NULL");
+  }
+  std::string e =
+      p->st.init(d->page_tokens, d->pool_bytes, d->chunk_bytes, d->placement_seed, d->max_requests, virt);
   if (!e.empty()) {
     delete p;
     return fail(CP_EINVAL, "%s", e.c_str());
@@ -122,7 +244,13 @@ cp_status cp_pool_create(const cp_pool_desc *d, cp_pool **out) {
     DeviceGuard g(d->device);
     hipError_t he;
     uint64_t bytes = p->st.n_chunks() * p->st.chunk_bytes();
-    if (d->device_mem) {
+    if (virt) {
+      cp_status rc = vmm_setup(p, d->device);
+      if (rc) {
+        delete p;
+        return rc;
+      }
+    } else if (d->device_mem) {
       if ((uintptr_t)d->device_mem % 256) {
         delete p;
         return fail(CP_EINVAL, "device_mem must be 256-byte aligned");
@@ -160,6 +288,14 @@ cp_status cp_pool_destroy(cp_pool *p) {
   if (p->st.n_open() > 0) return fail(CP_ESTATE, "%d requests still open", p->st.n_open());
   if (!p->host_only) {
     DeviceGuard g(p->device);
+    if (p->vmm) {
+      (void)hipDeviceSynchronize();
+      for (auto &kv : p->vmm_handles) {
+        (void)hipMemUnmap(p->dev_pool + (uint64_t)kv.first * p->st.chunk_bytes(), p->st.chunk_bytes());
+        (void)hipMemRelease(kv.second);
+      }
+      (void)hipMemAddressFree(p->dev_pool, p->st.span_bytes());
+    }
     if (p->owns_pool && p->dev_pool) (void)hipFree(p->dev_pool);
     if (p->dev_pte) (void)hipFree(p->dev_pte);
     if (p->pin_pte) (void)hipHostFree(p->pin_pte);
@@ -180,6 +316,9 @@ cp_status cp_pool_stats(cp_pool *p, cp_pool_stats_t *o) {
   o->pages_reserved = p->st.pages_reserved();
   o->requests_open = p->st.n_open();
   o->models = p->st.n_models();
+  o->span_bytes = p->st.span_bytes();
+  o->backing = p->st.virt() ? CP_BACKING_VIRTUAL : CP_BACKING_BUFFER;
+  o->max_models = p->st.max_models();
   return CP_OK;
 }
 
@@ -217,6 +356,7 @@ cp_status cp_request_open(cp_pool *p, int32_t model_id, int64_t reserve_tokens, 
   std::string err;
   int rc = p->st.open(model_id, reserve_tokens, req_id, &err);
   if (rc == -3) return fail(CP_ENOSPC, "%s", err.c_str());
+  if (rc == -2) return fail(CP_ENOMEM, "%s", err.c_str());
   if (rc != 0) return fail(CP_EINVAL, "%s", err.c_str());
   return CP_OK;
 }
@@ -224,7 +364,10 @@ cp_status cp_request_open(cp_pool *p, int32_t model_id, int64_t reserve_tokens, 
 cp_status cp_request_close(cp_pool *p, int32_t req_id) {
   if (!p) return fail(CP_EINVAL, "null pool");
   if (!p->st.valid_open(req_id)) return fail(CP_EINVAL, "request %d is not open", req_id);
+  p->vmm_synced = false;
+  p->vmm_err = hipSuccess;
   p->st.close(req_id);
+  if (p->vmm_err != hipSuccess) return hip_fail(p->vmm_err, "request closed, but unmapping its chunks failed");
   return CP_OK;
 }
 
@@ -367,7 +510,10 @@ cp_status cp_kv_append(cp_pool *p, int32_t n, const int32_t *req_ids, const int3
   if (total == 0) return CP_OK;
   if (total > 0x7FFFFFFF) return fail(CP_EINVAL, "too many rows in one call");
 
-  // All checks passed: allocate pages and update host page tables.
+  // All checks passed: carve (and map) chunks, then allocate pages and
+  // update host page tables.
+  rc = prepare_growth(p, n, req_ids, n_new);
+  if (rc) return rc;
   std::vector<uint32_t> old_len(n);
   uint64_t lo = UINT64_MAX, hi = 0;
   for (int32_t i = 0; i < n; ++i) {
@@ -842,6 +988,12 @@ cp_status cp_attn_decode_step(cp_pool *p, int32_t n, const int32_t *req_ids, con
   }
   if (any && !rows) return fail(CP_EINVAL, "null rows");
   if (!any) return cp_attn_decode_ex(p, n, req_ids, q, out, lse, hip_stream, opts);
+  uint64_t total_elems = 0;
+  for (int32_t i = 0; i < n; ++i)
+    if (n_new[i]) total_elems += (uint64_t)p->st.model(p->st.req(req_ids[i]).model).row_elems;
+  if (total_elems > 0xFFFFFFFFull) return fail(CP_EINVAL, "too many rows in one call");
+  rc = prepare_growth(p, n, req_ids, n_new);
+  if (rc) return rc;
 
   // Allocate the new pages on the host; their entries travel with the launch.
   std::vector<AppendPlan> plan(n);
@@ -861,7 +1013,6 @@ cp_status cp_attn_decode_step(cp_pool *p, int32_t n, const int32_t *req_ids, con
       hi = std::max(hi, first + count);
     }
     off += (uint64_t)row_elems;
-    if (off > 0xFFFFFFFFull) return fail(CP_EINVAL, "too many rows in one call");
   }
   rc = decode_impl(p, n, req_ids, q, out, lse, hip_stream, &o, rows, &plan);
   if (rc) {

@@ -55,7 +55,7 @@ void RangeAlloc::release(uint64_t start, uint64_t len) {
 // ------------------------------------------------------------- PoolState
 
 std::string PoolState::init(int32_t page_tokens, uint64_t pool_bytes, uint64_t chunk_bytes, uint64_t seed,
-                            int32_t max_requests) {
+                            int32_t max_requests, bool virt) {
   if (page_tokens < 1 || page_tokens > 4096) return "page_tokens must be in [1, 4096]";
   if (chunk_bytes == 0) chunk_bytes = 2ull << 20;
   if (chunk_bytes % 256) return "chunk_bytes must be a multiple of 256";
@@ -70,14 +70,27 @@ std::string PoolState::init(int32_t page_tokens, uint64_t pool_bytes, uint64_t c
   n_chunks_ = n;
   seed_ = seed;
   rng_ = SplitMix64(seed);
-  chunks_.assign(n, Chunk{});
+  virt_ = virt;
+  mapped_ = 0;
+  vfree_.clear();
+  vnext_.clear();
   free_heap_ = decltype(free_heap_)();
   free_rand_.clear();
-  if (seed) {
-    free_rand_.resize(n);
-    for (uint64_t i = 0; i < n; ++i) free_rand_[i] = (int32_t)i;
+  if (virt) {
+    // one budget-sized range of chunk slots per model, all of them
+    // addressable by 32-bit page entries; a model's slots are created when
+    // it registers (placement_seed plays no part: the driver places memory)
+    max_models_ = std::min<uint64_t>(16, (1ull << 40) / (n * chunk_bytes));
+    chunks_.clear();
   } else {
-    for (uint64_t i = 0; i < n; ++i) free_heap_.push((int32_t)i);
+    max_models_ = 16;
+    chunks_.assign(n, Chunk{});
+    if (seed) {
+      free_rand_.resize(n);
+      for (uint64_t i = 0; i < n; ++i) free_rand_[i] = (int32_t)i;
+    } else {
+      for (uint64_t i = 0; i < n; ++i) free_heap_.push((int32_t)i);
+    }
   }
   // The smallest page allowed is page_tokens * 128 bytes; page-table space
   // for twice the pages that could ever be carved leaves room for
@@ -99,6 +112,8 @@ std::string PoolState::init(int32_t page_tokens, uint64_t pool_bytes, uint64_t c
 
 std::string PoolState::add_model(const Geom &gi, int32_t *id) {
   if (models_.size() >= 16) return "at most 16 models per pool";
+  if (virt_ && models_.size() >= max_models_)
+    return "a virtual pool of this budget has address space for " + std::to_string(max_models_) + " models";
   Geom g = gi;
   if (g.hq < 1 || g.hq > 256) return "n_q_heads must be in [1, 256]";
   if (g.kind == kMLA) {
@@ -132,6 +147,11 @@ std::string PoolState::add_model(const Geom &gi, int32_t *id) {
   g.ppc = (int32_t)(chunk_bytes_ / (uint64_t)g.page_bytes);
   models_.push_back(g);
   acct_.push_back(ModelAcct{});
+  if (virt_) {
+    chunks_.resize(models_.size() * n_chunks_);
+    vfree_.emplace_back();
+    vnext_.push_back(0);
+  }
   *id = (int32_t)models_.size() - 1;
   return "";
 }
@@ -187,17 +207,29 @@ int PoolState::open(int32_t model, int64_t reserve_tokens, int32_t *id, std::str
   acct_[model].reserved += pages;
   ++n_open_;
   *id = rid;
+  if (virt_) {
+    // back the whole reservation now: admission is the slow path, and the
+    // growth of an admitted request then never maps memory
+    std::vector<int32_t> carved;
+    if (!ensure_slots(model, acct_[model].reserved - acct_[model].used, &carved)) {
+      close(rid);  // trims the chunks carved above
+      *err = "could not map physical memory for the reservation";
+      return -2;
+    }
+  }
   return 0;
 }
 
 void PoolState::close(int32_t id) {
   Request &r = reqs_[id];
+  const int32_t model = r.model;
   for (int64_t p = 0; p < r.pages_used; ++p) free_page(pte_[r.pte_base + p]);
-  acct_[r.model].reserved -= r.reserve_pages;
+  acct_[model].reserved -= r.reserve_pages;
   pte_ranges_.release(r.pte_base, (uint64_t)r.reserve_pages);
   r = Request{};
   free_ids_.push_back(id);
   --n_open_;
+  if (virt_) trim(model);
 }
 
 bool PoolState::fits_reservation(int32_t id, int64_t new_len) const {
@@ -215,7 +247,70 @@ void PoolState::grow(int32_t id, int64_t new_len, uint64_t *first, uint64_t *cou
   r.ctx_len = new_len;
 }
 
-int32_t PoolState::take_chunk() {
+int64_t PoolState::pages_to_grow(int32_t id, int64_t new_len) const {
+  const Request &r = reqs_[id];
+  int64_t need = ceil_div(new_len, P_);
+  return need > r.pages_used ? need - r.pages_used : 0;
+}
+
+bool PoolState::ensure_slots(int32_t model, int64_t pages, std::vector<int32_t> *carved) {
+  const Geom &g = models_[model];
+  ModelAcct &a = acct_[model];
+  while (a.held * g.ppc - a.used < pages) {
+    int32_t c = take_chunk(model);
+    if (c < 0) return false;
+    carve(c, model);
+    carved->push_back(c);
+  }
+  return true;
+}
+
+void PoolState::release_empty(const std::vector<int32_t> &carved) {
+  for (int32_t c : carved)
+    if (chunks_[c].model >= 0 && chunks_[c].used == 0) uncarve(c);
+}
+
+void PoolState::carve(int32_t c, int32_t model) {
+  const Geom &g = models_[model];
+  Chunk &ch = chunks_[c];
+  ch.model = model;
+  ch.used = 0;
+  ch.bits.assign((size_t)(g.ppc + 63) / 64, 0ull);
+  for (int32_t s = 0; s < g.ppc; ++s) ch.bits[s >> 6] |= 1ull << (s & 63);
+  acct_[model].held += 1;
+  acct_[model].partial[c] = g.ppc;
+}
+
+void PoolState::uncarve(int32_t c) {
+  Chunk &ch = chunks_[c];
+  ModelAcct &a = acct_[ch.model];
+  a.partial.erase(c);
+  a.held -= 1;
+  ch.model = -1;
+  ch.bits.clear();
+  give_chunk(c);
+}
+
+int32_t PoolState::take_chunk(int32_t model) {
+  if (virt_) {
+    if (mapped_ >= n_chunks_) return -1;
+    auto &fr = vfree_[model];
+    int32_t c;
+    bool reused = !fr.empty();
+    if (reused) {
+      c = fr.top();
+    } else {
+      if (vnext_[model] >= n_chunks_) return -1;  // unreachable: the range holds the whole budget
+      c = (int32_t)((uint64_t)model * n_chunks_ + vnext_[model]);
+    }
+    if (map_chunk && !map_chunk(c)) return -1;
+    if (reused)
+      fr.pop();
+    else
+      vnext_[model] += 1;
+    mapped_ += 1;
+    return c;
+  }
   if (seed_) {
     if (free_rand_.empty()) return -1;
     size_t i = (size_t)(rng_.next() % free_rand_.size());
@@ -231,6 +326,12 @@ int32_t PoolState::take_chunk() {
 }
 
 void PoolState::give_chunk(int32_t c) {
+  if (virt_) {
+    if (unmap_chunk) unmap_chunk(c);
+    mapped_ -= 1;
+    vfree_[(uint64_t)c / n_chunks_].push(c);
+    return;
+  }
   if (seed_)
     free_rand_.push_back(c);
   else
@@ -244,15 +345,10 @@ uint32_t PoolState::alloc_page(int32_t model) {
   if (!a.partial.empty()) {
     c = a.partial.begin()->first;
   } else {
-    c = take_chunk();
-    if (c < 0) return 0xFFFFFFFFu;  // unreachable for admitted requests
-    Chunk &ch = chunks_[c];
-    ch.model = model;
-    ch.used = 0;
-    ch.bits.assign((size_t)(g.ppc + 63) / 64, 0ull);
-    for (int32_t s = 0; s < g.ppc; ++s) ch.bits[s >> 6] |= 1ull << (s & 63);
-    a.held += 1;
-    a.partial[c] = g.ppc;
+    // unreachable: ensure_slots carved every chunk this growth needs
+    c = take_chunk(model);
+    if (c < 0) return 0xFFFFFFFFu;
+    carve(c, model);
   }
   Chunk &ch = chunks_[c];
   int32_t slot = -1;
@@ -280,14 +376,22 @@ void PoolState::free_page(uint32_t pte) {
   ch.bits[slot >> 6] |= 1ull << (slot & 63);
   ch.used -= 1;
   a.used -= 1;
-  if (ch.used == 0) {
-    a.partial.erase(c);
-    a.held -= 1;
-    ch.model = -1;
-    ch.bits.clear();
-    give_chunk(c);
+  if (ch.used == 0 && !virt_) {
+    uncarve(c);
   } else {
-    a.partial[c] += 1;
+    a.partial[c] += 1;  // a virtual pool's empty chunks wait for trim
+  }
+}
+
+void PoolState::trim(int32_t model) {
+  const Geom &g = models_[model];
+  ModelAcct &a = acct_[model];
+  std::vector<int32_t> empty;
+  for (auto it = a.partial.rbegin(); it != a.partial.rend(); ++it)
+    if (chunks_[it->first].used == 0) empty.push_back(it->first);
+  for (int32_t c : empty) {  // highest slots first
+    if ((a.held - 1) * g.ppc < a.reserved) break;  // the remaining slots are still owed
+    uncarve(c);
   }
 }
 

@@ -9,9 +9,18 @@
 // page sizes inside a chunk (Section 3.1: one pool page budget across
 // heterogeneous models; Section 2.3 C1). A page holds page_tokens tokens.
 // A page-table entry (PTE) is the page's byte offset in the pool >> 8.
+//
+// Two backings share this bookkeeping. Buffer: the chunks are the n_chunks
+// consecutive slices of one device buffer. Virtual (Section 3.1, "KV-cache
+// Planner and Virtualizer"; Section 4, KV-cache virtualization): each model
+// owns a contiguous range of n_chunks chunk slots in one reserved address
+// span, and a slot is backed by physical memory only while it holds pages;
+// the budget caps the number of backed slots, not the span. The mapping
+// itself is done through the map_chunk / unmap_chunk hooks.
 #pragma once
 
 #include <cstdint>
+#include <functional>
 #include <map>
 #include <queue>
 #include <string>
@@ -71,13 +80,24 @@ class PoolState {
  public:
   // Returns "" on success, or an error message.
   std::string init(int32_t page_tokens, uint64_t pool_bytes, uint64_t chunk_bytes, uint64_t seed,
-                   int32_t max_requests);
+                   int32_t max_requests, bool virt = false);
 
   int32_t page_tokens() const { return P_; }
   uint64_t chunk_bytes() const { return chunk_bytes_; }
   uint64_t n_chunks() const { return n_chunks_; }
   uint64_t pte_capacity() const { return pte_.size(); }
   uint64_t pool_bytes_used() const { return n_chunks_ * chunk_bytes_; }
+  bool virt() const { return virt_; }
+  // Bytes of address space the page-table entries can point into: the
+  // buffer, or for a virtual pool one budget-sized range per model slot.
+  uint64_t span_bytes() const { return (virt_ ? max_models_ * n_chunks_ : n_chunks_) * chunk_bytes_; }
+  int32_t max_models() const { return (int32_t)max_models_; }
+
+  // Virtual pools: back / release chunk slot c (byte offset c * chunk_bytes
+  // in the span). map_chunk returns false if no physical memory could be
+  // mapped. Unset hooks do nothing (host-only pools).
+  std::function<bool(int32_t)> map_chunk;
+  std::function<void(int32_t)> unmap_chunk;
 
   // Models.
   std::string add_model(const Geom &g_in, int32_t *id);
@@ -88,7 +108,11 @@ class PoolState {
   int32_t max_requests() const { return (int32_t)reqs_.size(); }
   bool valid_open(int32_t id) const { return id >= 0 && id < (int32_t)reqs_.size() && reqs_[id].open; }
   const Request &req(int32_t id) const { return reqs_[id]; }
-  // Admission (returns 0, or -3 for budget exhausted, -1 for bad args).
+  // Admission (returns 0, or -3 for budget exhausted, -1 for bad args, -2
+  // when a virtual pool could not map the reservation's chunks). A virtual
+  // pool backs the whole reservation at admission and keeps a model's
+  // chunks while its open reservations may need their slots, so the growth
+  // of admitted requests never maps or unmaps memory.
   int open(int32_t model, int64_t reserve_tokens, int32_t *id, std::string *err);
   void close(int32_t id);
   int32_t n_open() const { return n_open_; }
@@ -101,6 +125,15 @@ class PoolState {
   // as [*first, *first + *count). Never fails for admitted requests within
   // their reservation.
   void grow(int32_t id, int64_t new_len, uint64_t *first, uint64_t *count);
+  // Pages request id still needs to reach new_len tokens.
+  int64_t pages_to_grow(int32_t id, int64_t new_len) const;
+  // Carves fresh chunks for a model until it has at least `pages` free page
+  // slots, appending each to *carved. Returns false if a chunk could not be
+  // taken or mapped; the caller then gives the carved chunks back with
+  // release_empty. Run before grow, so that grow itself cannot fail.
+  bool ensure_slots(int32_t model, int64_t pages, std::vector<int32_t> *carved);
+  // Returns chunks of *carved that hold no pages to the free list.
+  void release_empty(const std::vector<int32_t> &carved);
 
   const uint32_t *pte_mirror() const { return pte_.data(); }
   uint32_t *pte_mirror_mut() { return pte_.data(); }
@@ -125,9 +158,16 @@ class PoolState {
     std::map<int32_t, int32_t> partial;  // chunk -> free slots (chunks with room)
   };
 
-  uint64_t free_count() const { return seed_ ? free_rand_.size() : free_heap_.size(); }
-  int32_t take_chunk();
+  uint64_t free_count() const {
+    return virt_ ? n_chunks_ - mapped_ : (seed_ ? free_rand_.size() : free_heap_.size());
+  }
+  int32_t take_chunk(int32_t model);
   void give_chunk(int32_t c);
+  void carve(int32_t c, int32_t model);
+  void uncarve(int32_t c);
+  // virtual pools: release a model's empty chunks that no open reservation
+  // still needs, highest slots first
+  void trim(int32_t model);
   uint32_t alloc_page(int32_t model);
   void free_page(uint32_t pte);
 
@@ -137,6 +177,12 @@ class PoolState {
   std::vector<Chunk> chunks_;
   std::priority_queue<int32_t, std::vector<int32_t>, std::greater<int32_t>> free_heap_;
   std::vector<int32_t> free_rand_;
+  // virtual pools: per model, slots given back (lowest first) and the next
+  // never-used slot of its range
+  bool virt_ = false;
+  uint64_t max_models_ = 16, mapped_ = 0;
+  std::vector<std::priority_queue<int32_t, std::vector<int32_t>, std::greater<int32_t>>> vfree_;
+  std::vector<uint64_t> vnext_;
   std::vector<Geom> models_;
   std::vector<ModelAcct> acct_;
   std::vector<Request> reqs_;

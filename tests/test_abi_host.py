@@ -247,3 +247,149 @@ def test_random_admission_never_strands_admitted_requests():
         p.close(r)
     assert p.stats()["chunks_used"] == 0
     p.destroy()
+
+
+# ---------------------------------------------------------------- virtual pools
+# Host-only virtual pools run the same bookkeeping as device ones (address
+# ranges per model, budget on mapped chunks) with the mapping calls left out.
+
+def virtual_pool(pool_bytes=32 << 20, chunk=2 << 20, page_tokens=64, max_requests=0):
+    return cpl.Pool(page_tokens=page_tokens, pool_bytes=pool_bytes, chunk_bytes=chunk, device=-1,
+                    max_requests=max_requests, backing=cpl.CP_BACKING_VIRTUAL)
+
+
+def test_virtual_pool_gives_each_model_its_own_range():
+    chunk, n = 2 << 20, 16
+    p = virtual_pool(pool_bytes=n * chunk, chunk=chunk)
+    s = p.stats()
+    assert s["backing"] == cpl.CP_BACKING_VIRTUAL and s["max_models"] == 16
+    assert s["span_bytes"] == 16 * n * chunk
+    mids = reg_all(p)
+    lens = [3000, 2500, 900]
+    rids = [p.open(m, L) for m, L in zip(mids, lens)]
+    # admission maps the chunks of each whole reservation
+    need = [math.ceil(math.ceil(L / 64) / p.info(m)["pages_per_chunk"]) for m, L in zip(mids, lens)]
+    assert p.stats()["chunks_used"] == sum(need)
+    p.append(rids, lens, None)
+    assert p.stats()["chunks_used"] == sum(need)  # growth maps nothing
+    for m, r, L, k in zip(mids, rids, lens, need):
+        pb, ppc = p.info(m)["page_bytes"], p.info(m)["pages_per_chunk"]
+        slots = set()
+        for e in p.pages(r):
+            ch, slot, rem = pte_to_chunk_slot(e, chunk, pb)
+            assert rem == 0 and slot < ppc
+            assert m * n <= ch < (m + 1) * n, "pages of model m lie in its own range"
+            slots.add((ch, slot))
+        assert len(slots) == math.ceil(L / 64)
+        # a model's chunks fill its range from the bottom, slots in order
+        assert sorted({c for c, _ in slots}) == list(range(m * n, m * n + k))
+    p.close(rids[0])
+    assert p.stats()["chunks_used"] == sum(need) - need[0]
+    # a released slot is the first reused
+    r = p.open(mids[0], 64)
+    p.append([r], [1], None)
+    assert pte_to_chunk_slot(p.pages(r)[0], chunk, p.info(mids[0])["page_bytes"])[:2] == (mids[0] * n, 0)
+    for x in [r] + rids[1:]:
+        p.close(x)
+    assert p.stats()["chunks_used"] == 0
+    p.destroy()
+
+
+def test_virtual_pool_keeps_chunks_other_reservations_need():
+    chunk = 2 << 20
+    p = virtual_pool(pool_bytes=16 * chunk, chunk=chunk)
+    a = p.register_spec(MLA16)
+    ppc = p.info(a)["pages_per_chunk"]
+    r1 = p.open(a, ppc * 64)        # one chunk
+    r2 = p.open(a, ppc * 64 // 2)   # half a chunk: a second chunk
+    assert p.stats()["chunks_used"] == 2
+    p.append([r1, r2], [ppc * 64, 64], None)  # r1 fills chunk 0, r2 starts chunk 1
+    p.close(r1)  # chunk 0 empties, but r2 is owed ppc/2 - 1 more pages: one chunk stays
+    assert p.stats()["chunks_used"] == 1
+    p.append([r2], [ppc * 64 // 2 - 64], None)  # grows into its reservation without mapping
+    assert p.stats()["chunks_used"] == 1
+    p.close(r2)
+    assert p.stats()["chunks_used"] == 0
+    p.destroy()
+
+
+def test_virtual_pool_budget_caps_mapped_chunks():
+    chunk = 2 << 20
+    p = virtual_pool(pool_bytes=4 * chunk, chunk=chunk)
+    a, b, c = reg_all(p)
+    ppc_a = p.info(a)["pages_per_chunk"]
+    ra = p.open(a, 3 * ppc_a * 64)  # three chunks of model a, mapped at admission
+    assert p.stats()["chunks_used"] == 3
+    before = p.stats()
+    with pytest.raises(cpl.CrossPoolError) as e:
+        p.open(c, 2 * p.info(c)["pages_per_chunk"] * 64)  # two more chunks: over the budget
+    assert e.value.status == cpl.CP_ENOSPC and p.stats() == before
+    rc = p.open(c, 64)
+    assert p.stats()["chunks_used"] == 4 == p.stats()["chunks_total"]
+    p.append([ra, rc], [3 * ppc_a * 64, 64], None)
+    assert p.stats()["chunks_used"] == 4
+    p.close(ra)
+    assert p.stats()["chunks_used"] == 1
+    p.close(rc)
+    p.destroy()
+
+
+def test_virtual_pool_model_count_follows_the_address_limit():
+    # 256 GiB budget: four 256 GiB ranges fill the 1 TiB that page entries reach
+    p = virtual_pool(pool_bytes=256 << 30, chunk=64 << 20, page_tokens=4096)
+    assert p.stats()["max_models"] == 4
+    for _ in range(4):
+        p.register_spec(MQA32)
+    with pytest.raises(cpl.CrossPoolError, match="address space for 4 models"):
+        p.register_spec(MQA32)
+    p.destroy()
+
+
+def test_virtual_pool_create_validation():
+    with pytest.raises(cpl.CrossPoolError, match="device_mem must be NULL"):
+        cpl.Pool(page_tokens=64, pool_bytes=8 << 20, device=-1, device_mem=1 << 20, backing=cpl.CP_BACKING_VIRTUAL)
+    with pytest.raises(cpl.CrossPoolError, match="unknown backing"):
+        cpl.Pool(page_tokens=64, pool_bytes=8 << 20, device=-1, backing=7)
+
+
+@pytest.mark.parametrize("backing", [cpl.CP_BACKING_BUFFER, cpl.CP_BACKING_VIRTUAL])
+def test_random_traffic_invariants_both_backings(backing):
+    """Open / append / close traffic: admitted requests always fill their
+    reservations, rejections change nothing, mapped chunks never exceed the
+    budget, and every chunk comes back at the end."""
+    rng = np.random.default_rng(321)
+    chunk = 2 << 20
+    p = cpl.Pool(page_tokens=64, pool_bytes=20 * chunk, chunk_bytes=chunk, device=-1, placement_seed=5,
+                 backing=backing)
+    mids = reg_all(p)
+    live = {}
+    for step in range(500):
+        op = rng.integers(0, 3)
+        if op == 0 or not live:
+            m = int(rng.integers(0, 3))
+            before = p.stats()
+            try:
+                r = p.open(mids[m], int(rng.integers(1, 7000)))
+                live[r] = (m, p.stats()["pages_reserved"] - before["pages_reserved"])
+            except cpl.CrossPoolError as e:
+                assert e.status == cpl.CP_ENOSPC and p.stats() == before
+        elif op == 1:
+            r = int(rng.choice(list(live)))
+            room = live[r][1] * 64 - p.ctx_len(r)
+            if room > 0:
+                p.append([r], [int(rng.integers(1, room + 1))], None)
+        else:
+            r = int(rng.choice(list(live)))
+            p.close(r)
+            del live[r]
+        s = p.stats()
+        assert s["chunks_used"] <= s["chunks_total"]
+        assert s["pages_used"] == sum(math.ceil(p.ctx_len(r) / 64) for r in live)
+    for r, (m, pages) in live.items():
+        room = pages * 64 - p.ctx_len(r)
+        if room:
+            p.append([r], [room], None)
+    for r in list(live):
+        p.close(r)
+    assert p.stats()["chunks_used"] == 0
+    p.destroy()

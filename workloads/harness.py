@@ -41,6 +41,9 @@ class Loaded:
         return self.lse[off:off + self.workload.model(r).n_q_heads].cpu().numpy().astype(np.float64)
 
     def close(self):
+        import torch
+
+        torch.cuda.synchronize()  # no queued kernel may still read the pages
         for r in self.req_ids + self.fillers:
             self.pool.close(r)
         self.pool.destroy()
@@ -54,12 +57,13 @@ def to_device_u16(arr: np.ndarray, device):
 
 def load(wl: Workload, device: int = 0, *, placement_seed: Optional[int] = None, reserve_extra: int = 0,
          interleave: int = 0, rows_override: Optional[Dict[int, np.ndarray]] = None,
-         q_override: Optional[List[np.ndarray]] = None, chunk_rows: int = 1 << 17) -> Loaded:
+         q_override: Optional[List[np.ndarray]] = None, chunk_rows: int = 1 << 17, backing: int = 0) -> Loaded:
     """Build a pool holding the workload.
 
     interleave > 0 appends rows in rounds of `interleave` tokens per request,
     so physical pages of different requests alternate. rows_override maps a
     request index to its rows (uint16 bits) instead of the seeded draw.
+    backing selects the pool's memory (0 one buffer, 1 virtual ranges).
     """
     import torch
 
@@ -68,7 +72,7 @@ def load(wl: Workload, device: int = 0, *, placement_seed: Optional[int] = None,
     dev = torch.device("cuda", device)
     seed = wl.placement_seed if placement_seed is None else placement_seed
     pool = cpl.Pool(page_tokens=PAGE_TOKENS, pool_bytes=wl.pool_bytes, chunk_bytes=wl.chunk_bytes,
-                    placement_seed=seed, device=device)
+                    placement_seed=seed, device=device, backing=backing)
     mids = {name: pool.register_spec(MODELS[name]) for name in wl.models_used()}
     if wl.filler_model and wl.filler_model not in mids:
         mids[wl.filler_model] = pool.register_spec(MODELS[wl.filler_model])
