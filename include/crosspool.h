@@ -164,6 +164,12 @@ typedef struct {
   int32_t rope_dim;    /* MLA: decoupled rope width; K width = latent + rope */
   float softmax_scale; /* > 0; 0 means 1/sqrt(head_dim) for GQA (required for MLA) */
   int32_t dtype;       /* cp_dtype; only CP_BF16 */
+  /* Attention layers whose KV the pool holds, in [1, 1024]; 0 means 1.
+   * Each layer has its own KV plane: a request owns one page set per layer,
+   * all holding the same token positions, and a decode step reads the
+   * plane of the request's current layer (Section 3.2, layer cursor). The
+   * geometry above is that of one layer; the budget counts every plane. */
+  int32_t n_layers;
 } cp_model_desc;
 
 /* Register the KV geometry of one attention layer of a model (Section 2.3
@@ -180,6 +186,7 @@ typedef struct {
   int32_t page_bytes;        /* page_tokens * kappa */
   int32_t pages_per_chunk;   /* pages carved from one chunk */
   int32_t row_elems;         /* bf16 elements in one logical row */
+  int32_t n_layers;          /* KV planes per request */
 } cp_model_info_t;
 
 cp_status cp_model_info(cp_pool *pool, int32_t model_id, cp_model_info_t *out);
@@ -206,11 +213,20 @@ cp_status cp_request_open(cp_pool *pool, int32_t model_id, int64_t reserve_token
  * synchronisation per call. */
 cp_status cp_request_close(cp_pool *pool, int32_t req_id);
 
+/* Committed tokens of the request: those present in every layer's plane
+ * (a token in flight through the layers is not counted until its last
+ * layer's decode step). */
 cp_status cp_request_len(cp_pool *pool, int32_t req_id, int64_t *ctx_len);
 
-/* Copy the request's page-table entries [first, first + count) to host
- * memory. An entry is the byte offset of the page inside the pool buffer,
- * shifted right by 8. For tests and debugging. */
+/* The request's layer cursor (Section 3.2): the layer its next decode step
+ * reads, in [0, n_layers), and whether a new token is in flight (placed at
+ * the first layer's step, committed after the last layer's). */
+cp_status cp_request_cursor(cp_pool *pool, int32_t req_id, int32_t *layer, int32_t *in_flight);
+
+/* Copy the request's page-table entries of pages [first, first + count) to
+ * host memory, for every layer: ptes is [n_layers][count]. An entry is the
+ * byte offset of the page inside the pool's address span, shifted right by
+ * 8. For tests and debugging. */
 cp_status cp_request_pages(cp_pool *pool, int32_t req_id, int64_t first, int64_t count, uint32_t *ptes);
 
 /* ------------------------------------------------------------------- KV */
@@ -220,10 +236,13 @@ cp_status cp_request_pages(cp_pool *pool, int32_t req_id, int64_t first, int64_t
  * a normal paged interface while physical pages are mapped on demand).
  *
  * rows: device memory, the requests' logical rows packed in call order,
- *   request i contributing n_new[i] consecutive rows. A logical row is
+ *   request i contributing n_layers * n_new[i] rows: [n_layers][n_new[i]]
+ *   (layer-major; one layer for single-layer models). A logical row is
  *   row_elems bf16 values: MLA [latent | rope]; GQA/MQA [K head 0 .. K head
  *   Hkv-1 | V head 0 .. V head Hkv-1], each head head_dim wide. Rows are
- *   copied bit for bit.
+ *   copied bit for bit. The tokens are committed at once in every layer, so
+ *   a request with a token in flight (cursor past the first layer) cannot
+ *   append (CP_EINVAL).
  * req_ids, n_new: host arrays of n entries; req_ids must be distinct;
  *   n_new[i] >= 0.
  * New pages come from the model's slab, or a fresh chunk of the shared
@@ -247,7 +266,10 @@ cp_status cp_kv_append(cp_pool *pool, int32_t n, const int32_t *req_ids, const i
  * lse: device, per request [n_q_heads] float, packed in call order.
  * req_ids: host array of n distinct ids, n >= 1.
  * Accumulation is fp32; outputs depend only on the logical KV, never on
- * the physical placement of pages (bit-identical across placements).
+ * the physical placement of pages (bit-identical across placements). For a
+ * multi-layer model, K and V are those of the request's current layer
+ * (cp_request_cursor) and the context includes a token in flight; this call
+ * does not move the cursor.
  * Errors: CP_EINVAL (unknown or duplicate id, empty context), CP_ESTATE
  * (host-only pool), CP_ENOMEM (workspace growth failed), CP_EHIP. */
 cp_status cp_attn_decode(cp_pool *pool, int32_t n, const int32_t *req_ids, const void *q, void *out, float *lse,
@@ -309,19 +331,31 @@ cp_status cp_attn_decode_ex(cp_pool *pool, int32_t n, const int32_t *req_ids, co
  * Pages for the new tokens are allocated on the host as in cp_kv_append; the
  * entry of a new page is passed to the launch, and every workgroup that reads
  * a request's last page writes that entry and the new row before reading it.
+ *
+ * Multi-layer models (Section 3.2, layer-wise pipeline: each batch keeps its
+ * own layer cursor, and requests of different models at different layers
+ * share one launch): a step serves each request at its current layer and
+ * then moves the cursor on. At the first layer, n_new = 1 places a new token
+ * (pages of every layer's plane are allocated; a multi-layer model's other
+ * planes get their new entries by one page-table copy) and its row of that
+ * layer is written; at later layers n_new must be 1 while the token is in
+ * flight (its row of that layer) and 0 otherwise. The token is committed
+ * after the last layer's step. A single-layer model commits at once, which
+ * is the behaviour described above.
  * Errors: those of cp_kv_append and cp_attn_decode_ex, plus CP_EINVAL for an
- * n_new other than 0 or 1. Argument and capacity checks run before any state
- * changes; if the attention launch fails once pages are allocated, the rows
- * are still appended (as by cp_kv_append) and the error is returned. */
+ * n_new other than 0 or 1 or not matching the token in flight. Argument and
+ * capacity checks run before any state changes; if the attention launch
+ * fails once pages are allocated, the rows are still appended (as by
+ * cp_kv_append), the cursors move on, and the error is returned. */
 cp_status cp_attn_decode_step(cp_pool *pool, int32_t n, const int32_t *req_ids, const int32_t *n_new,
                               const void *rows, const void *q, void *out, float *lse, void *hip_stream,
                               const cp_decode_opts *opts);
 
 /* Copy logical rows [start, start + n_tok) of one request out of the pool
- * into dst (device, n_tok * row_elems bf16), through the same page-table
- * translation that decode uses. Bit-exact inverse of cp_kv_append.
- * Errors: CP_EINVAL (range outside [0, ctx_len)), CP_ESTATE (host-only
- * pool), CP_EHIP. */
+ * into dst (device, [n_layers][n_tok][row_elems] bf16), through the same
+ * page-table translation that decode uses. Bit-exact inverse of
+ * cp_kv_append. Errors: CP_EINVAL (range outside the committed [0,
+ * ctx_len)), CP_ESTATE (host-only pool), CP_EHIP. */
 cp_status cp_kv_gather(cp_pool *pool, int32_t req_id, int64_t start, int64_t n_tok, void *dst, void *hip_stream);
 
 /* ---------------------------------------------------------------------

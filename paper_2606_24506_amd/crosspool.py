@@ -69,6 +69,7 @@ class cp_model_desc(C.Structure):
         ("rope_dim", C.c_int32),
         ("softmax_scale", C.c_float),
         ("dtype", C.c_int32),
+        ("n_layers", C.c_int32),
     ]
 
 
@@ -80,6 +81,7 @@ class cp_model_info_t(C.Structure):
         ("page_bytes", C.c_int32),
         ("pages_per_chunk", C.c_int32),
         ("row_elems", C.c_int32),
+        ("n_layers", C.c_int32),
     ]
 
 
@@ -133,6 +135,7 @@ def _load() -> C.CDLL:
         "cp_request_open": ([P, I32, I64, C.POINTER(I32)], I32),
         "cp_request_close": ([P, I32], I32),
         "cp_request_len": ([P, I32, C.POINTER(I64)], I32),
+        "cp_request_cursor": ([P, I32, C.POINTER(I32), C.POINTER(I32)], I32),
         "cp_request_pages": ([P, I32, I64, I64, C.POINTER(C.c_uint32)], I32),
         "cp_kv_append": ([P, I32, C.POINTER(I32), C.POINTER(I32), VP, VP], I32),
         "cp_attn_decode": ([P, I32, C.POINTER(I32), VP, VP, VP, VP], I32),
@@ -211,8 +214,8 @@ def cp_pool_stats(pool: int) -> dict:
 
 
 def cp_model_register(pool: int, kind: int, n_q_heads: int, n_kv_heads: int, head_dim: int = 0,
-                      latent_dim: int = 0, rope_dim: int = 0, softmax_scale: float = 0.0) -> int:
-    m = cp_model_desc(kind, n_q_heads, n_kv_heads, head_dim, latent_dim, rope_dim, softmax_scale, 0)
+                      latent_dim: int = 0, rope_dim: int = 0, softmax_scale: float = 0.0, n_layers: int = 1) -> int:
+    m = cp_model_desc(kind, n_q_heads, n_kv_heads, head_dim, latent_dim, rope_dim, softmax_scale, 0, n_layers)
     mid = C.c_int32()
     _check(LIB.cp_model_register(pool, C.byref(m), C.byref(mid)))
     return mid.value
@@ -240,10 +243,18 @@ def cp_request_len(pool: int, req_id: int) -> int:
     return n.value
 
 
-def cp_request_pages(pool: int, req_id: int, first: int, count: int) -> np.ndarray:
-    out = np.zeros(count, dtype=np.uint32)
+def cp_request_cursor(pool: int, req_id: int):
+    """(layer, in_flight) of the request's layer cursor."""
+    layer, inflight = C.c_int32(), C.c_int32()
+    _check(LIB.cp_request_cursor(pool, req_id, C.byref(layer), C.byref(inflight)))
+    return layer.value, inflight.value
+
+
+def cp_request_pages(pool: int, req_id: int, first: int, count: int, layers: int = 1) -> np.ndarray:
+    """Page-table entries, [count] for one layer or [layers][count]."""
+    out = np.zeros((layers, count), dtype=np.uint32)
     _check(LIB.cp_request_pages(pool, req_id, first, count, out.ctypes.data_as(C.POINTER(C.c_uint32))))
-    return out
+    return out[0] if layers == 1 else out
 
 
 def cp_kv_append(pool: int, req_ids: Sequence[int], n_new: Sequence[int], rows, stream=None) -> None:
@@ -323,13 +334,13 @@ class Pool:
     def register(self, kind: int, n_q_heads: int, n_kv_heads: int, **kw) -> int:
         return cp_model_register(self.handle, kind, n_q_heads, n_kv_heads, **kw)
 
-    def register_spec(self, spec) -> int:
+    def register_spec(self, spec, n_layers: int = 1) -> int:
         """Register a model described by an object with kind / head fields."""
         if spec.kind == "mla":
             return self.register(CP_KIND_MLA, spec.n_q_heads, 1, latent_dim=spec.latent_dim,
-                                 rope_dim=spec.rope_dim, softmax_scale=spec.scale)
+                                 rope_dim=spec.rope_dim, softmax_scale=spec.scale, n_layers=n_layers)
         return self.register(CP_KIND_GQA, spec.n_q_heads, spec.n_kv_heads, head_dim=spec.head_dim,
-                             softmax_scale=spec.scale)
+                             softmax_scale=spec.scale, n_layers=n_layers)
 
     def info(self, model_id: int) -> dict:
         return cp_model_info(self.handle, model_id)
@@ -343,10 +354,13 @@ class Pool:
     def ctx_len(self, req_id: int) -> int:
         return cp_request_len(self.handle, req_id)
 
-    def pages(self, req_id: int, first: int = 0, count: Optional[int] = None) -> np.ndarray:
+    def cursor(self, req_id: int):
+        return cp_request_cursor(self.handle, req_id)
+
+    def pages(self, req_id: int, first: int = 0, count: Optional[int] = None, layers: int = 1) -> np.ndarray:
         if count is None:
             count = -(-self.ctx_len(req_id) // self.page_tokens) - first
-        return cp_request_pages(self.handle, req_id, first, count)
+        return cp_request_pages(self.handle, req_id, first, count, layers)
 
     def stats(self) -> dict:
         return cp_pool_stats(self.handle)

@@ -333,6 +333,7 @@ cp_status cp_model_register(cp_pool *p, const cp_model_desc *m, int32_t *model_i
   g.latent = m->latent_dim;
   g.rope = m->rope_dim;
   g.scale = m->softmax_scale;
+  g.layers = m->n_layers == 0 ? 1 : m->n_layers;
   std::string e = p->st.add_model(g, model_id);
   if (!e.empty()) return fail(CP_EINVAL, "%s", e.c_str());
   return CP_OK;
@@ -348,6 +349,7 @@ cp_status cp_model_info(cp_pool *p, int32_t id, cp_model_info_t *o) {
   o->page_bytes = (int32_t)g.page_bytes;
   o->pages_per_chunk = g.ppc;
   o->row_elems = g.row_elems;
+  o->n_layers = g.layers;
   return CP_OK;
 }
 
@@ -378,6 +380,14 @@ cp_status cp_request_len(cp_pool *p, int32_t req_id, int64_t *ctx_len) {
   return CP_OK;
 }
 
+cp_status cp_request_cursor(cp_pool *p, int32_t req_id, int32_t *layer, int32_t *in_flight) {
+  if (!p || !layer || !in_flight) return fail(CP_EINVAL, "null argument");
+  if (!p->st.valid_open(req_id)) return fail(CP_EINVAL, "request %d is not open", req_id);
+  *layer = p->st.req(req_id).cursor;
+  *in_flight = p->st.req(req_id).inflight;
+  return CP_OK;
+}
+
 cp_status cp_request_pages(cp_pool *p, int32_t req_id, int64_t first, int64_t count, uint32_t *ptes) {
   if (!p || (!ptes && count > 0)) return fail(CP_EINVAL, "null argument");
   if (!p->st.valid_open(req_id)) return fail(CP_EINVAL, "request %d is not open", req_id);
@@ -385,7 +395,8 @@ cp_status cp_request_pages(cp_pool *p, int32_t req_id, int64_t first, int64_t co
   if (first < 0 || count < 0 || first + count > r.pages_used)
     return fail(CP_EINVAL, "page range [%lld, %lld) outside the %lld used pages", (long long)first,
                 (long long)(first + count), (long long)r.pages_used);
-  std::memcpy(ptes, p->st.pte_mirror() + r.pte_base + first, (size_t)count * 4);
+  for (int32_t l = 0; l < r.layers; ++l)  // [layers][count]
+    std::memcpy(ptes + (size_t)l * (size_t)count, p->st.pte_mirror() + r.plane_base(l) + first, (size_t)count * 4);
   return CP_OK;
 }
 
@@ -434,15 +445,20 @@ cp_status push_ptes(cp_pool *p, uint64_t lo, uint64_t hi, hipStream_t s) {
 }
 
 
-// Append launches for rows already accounted for in the host tables
-// (old_len[i]: context length before request i's new rows).
-cp_status launch_appends(cp_pool *p, int32_t n, const int32_t *req_ids, const int32_t *n_new, const void *rows,
-                         const uint32_t *old_len, hipStream_t s) {
-  // groups of at most kMaxReqPerLaunch requests and kMaxLaunchModels models.
+// One request's rows of one KV plane for launch_appends.
+struct AppItem {
+  int32_t model;
+  uint32_t n_new, old_len;  // rows, and the tokens already in the plane
+  uint32_t pte_base;        // the plane's first page-table entry
+  uint64_t src_off;         // element offset of the first row in `rows`
+};
+
+// Append launches for rows already accounted for in the host tables, in
+// groups of at most kMaxReqPerLaunch items and kMaxLaunchModels models.
+cp_status launch_appends(cp_pool *p, const std::vector<AppItem> &items, const void *rows, hipStream_t s) {
   const int32_t P = p->st.page_tokens();
-  uint64_t src = 0;  // element offset of the current request's rows
-  int32_t i = 0;
-  while (i < n) {
+  size_t i = 0;
+  while (i < items.size()) {
     AppendArgs a{};
     a.pool = p->dev_pool;
     a.pte = p->dev_pte;
@@ -450,26 +466,24 @@ cp_status launch_appends(cp_pool *p, int32_t n, const int32_t *req_ids, const in
     int32_t nm = 0, model_map[16];
     for (int k = 0; k < 16; ++k) model_map[k] = -1;
     uint32_t grid_rows = 0;
-    while (i < n && a.n_req < kMaxReqPerLaunch) {
-      const Request &r = p->st.req(req_ids[i]);
-      int32_t mi = model_map[r.model];
+    while (i < items.size() && a.n_req < kMaxReqPerLaunch) {
+      const AppItem &it = items[i];
+      int32_t mi = model_map[it.model];
       if (mi < 0) {
         if (nm == kMaxLaunchModels) break;
-        mi = model_map[r.model] = nm;
-        a.geom[nm++] = geom_k(p->st.model(r.model), P);
+        mi = model_map[it.model] = nm;
+        a.geom[nm++] = geom_k(p->st.model(it.model), P);
       }
-      const Geom &gm = p->st.model(r.model);
-      if (n_new[i] > 0) {
+      if (it.n_new > 0) {
         AppReq &q = a.req[a.n_req++];
-        q.src_off = src;
+        q.src_off = it.src_off;
         q.row_begin = grid_rows;
-        q.n_new = (uint32_t)n_new[i];
-        q.old_len = old_len[i];
-        q.pte_base = r.pte_base;
+        q.n_new = it.n_new;
+        q.old_len = it.old_len;
+        q.pte_base = it.pte_base;
         q.model = (uint32_t)mi;
-        grid_rows += (uint32_t)n_new[i];
+        grid_rows += it.n_new;
       }
-      src += (uint64_t)n_new[i] * (uint64_t)gm.row_elems;
       ++i;
     }
     a.total_rows = (int32_t)grid_rows;
@@ -495,12 +509,15 @@ cp_status cp_kv_append(cp_pool *p, int32_t n, const int32_t *req_ids, const int3
   for (int32_t i = 0; i < n; ++i) {
     if (n_new[i] < 0) return fail(CP_EINVAL, "negative n_new for request %d", req_ids[i]);
     const Request &r = p->st.req(req_ids[i]);
+    if (n_new[i] > 0 && (r.cursor != 0 || r.inflight))
+      return fail(CP_EINVAL, "request %d has a token in flight at layer %d; finish its decode steps first",
+                  req_ids[i], r.cursor);
     int64_t nl = r.ctx_len + n_new[i];
     if (nl > 0xFFFFFFF0ll) return fail(CP_EINVAL, "context length overflow");
     if (!p->st.fits_reservation(req_ids[i], nl))
       return fail(CP_EINVAL, "request %d would grow to %lld tokens, past its reservation of %lld pages", req_ids[i],
                   (long long)nl, (long long)r.reserve_pages);
-    total += n_new[i];
+    total += (int64_t)n_new[i] * r.layers;
   }
   if (p->host_only) {
     if (rows) return fail(CP_EINVAL, "host-only pool: rows must be NULL");
@@ -514,16 +531,22 @@ cp_status cp_kv_append(cp_pool *p, int32_t n, const int32_t *req_ids, const int3
   // update host page tables.
   rc = prepare_growth(p, n, req_ids, n_new);
   if (rc) return rc;
-  std::vector<uint32_t> old_len(n);
-  uint64_t lo = UINT64_MAX, hi = 0;
+  // Rows of request i are [layers][n_new][row_elems], requests in call order.
+  std::vector<AppItem> items;
+  uint64_t lo = UINT64_MAX, hi = 0, src = 0;
   for (int32_t i = 0; i < n; ++i) {
     const Request &r = p->st.req(req_ids[i]);
-    old_len[i] = (uint32_t)r.ctx_len;
+    const uint32_t old_len = (uint32_t)r.ctx_len;
+    const uint64_t row_elems = (uint64_t)p->st.model(r.model).row_elems;
     uint64_t first, count;
     p->st.grow(req_ids[i], r.ctx_len + n_new[i], &first, &count);
     if (count) {
       lo = std::min(lo, first);
       hi = std::max(hi, first + count);
+    }
+    for (int32_t l = 0; l < r.layers && n_new[i] > 0; ++l) {
+      items.push_back(AppItem{r.model, (uint32_t)n_new[i], old_len, r.plane_base(l), src});
+      src += (uint64_t)n_new[i] * row_elems;
     }
   }
   if (p->host_only) return CP_OK;
@@ -533,7 +556,7 @@ cp_status cp_kv_append(cp_pool *p, int32_t n, const int32_t *req_ids, const int3
   rc = push_ptes(p, lo, hi, s);
   if (rc) return rc;
 
-  return launch_appends(p, n, req_ids, n_new, rows, old_len.data(), s);
+  return launch_appends(p, items, rows, s);
 }
 
 cp_status cp_kv_gather(cp_pool *p, int32_t req_id, int64_t start, int64_t n_tok, void *dst, void *hip_stream) {
@@ -547,16 +570,19 @@ cp_status cp_kv_gather(cp_pool *p, int32_t req_id, int64_t start, int64_t n_tok,
   if (n_tok == 0) return CP_OK;
   if (!dst) return fail(CP_EINVAL, "null dst");
   DeviceGuard g(p->device);
-  GatherArgs a{};
-  a.pool = p->dev_pool;
-  a.pte = p->dev_pte;
-  a.dst = (uint16_t *)dst;
-  a.pte_base = r.pte_base;
-  a.start = (uint32_t)start;
-  a.n_tok = (uint32_t)n_tok;
-  a.geom = geom_k(p->st.model(r.model), p->st.page_tokens());
-  hipError_t e = launch_gather(a, (hipStream_t)hip_stream);
-  if (e != hipSuccess) return hip_fail(e, "gather launch");
+  const uint64_t row_elems = (uint64_t)p->st.model(r.model).row_elems;
+  for (int32_t l = 0; l < r.layers; ++l) {  // dst is [layers][n_tok][row_elems]
+    GatherArgs a{};
+    a.pool = p->dev_pool;
+    a.pte = p->dev_pte;
+    a.dst = (uint16_t *)dst + (uint64_t)l * (uint64_t)n_tok * row_elems;
+    a.pte_base = r.plane_base(l);
+    a.start = (uint32_t)start;
+    a.n_tok = (uint32_t)n_tok;
+    a.geom = geom_k(p->st.model(r.model), p->st.page_tokens());
+    hipError_t e = launch_gather(a, (hipStream_t)hip_stream);
+    if (e != hipSuccess) return hip_fail(e, "gather launch");
+  }
   return CP_OK;
 }
 
@@ -718,7 +744,7 @@ cp_status decode_impl(cp_pool *p, int32_t n, const int32_t *req_ids, const void 
   const int32_t P = p->st.page_tokens();
   for (int32_t i = 0; i < n; ++i) {
     const Request &r = p->st.req(req_ids[i]);
-    if (r.ctx_len < 1) return fail(CP_EINVAL, "request %d has an empty context", req_ids[i]);
+    if (r.attend_len() < 1) return fail(CP_EINVAL, "request %d has an empty context", req_ids[i]);
   }
 
   // Packed offsets in call order.
@@ -734,7 +760,7 @@ cp_status decode_impl(cp_pool *p, int32_t n, const int32_t *req_ids, const void 
     qo += (uint64_t)g.hq * g.d_k;
     oo += (uint64_t)g.hq * g.d_v;
     lo += (uint64_t)g.hq;
-    pages[i] = (r.ctx_len + P - 1) / P;
+    pages[i] = (r.attend_len() + P - 1) / P;
   }
   if (qo > 0xFFFFFFFFull || oo > 0xFFFFFFFFull) return fail(CP_EINVAL, "batch too large");
   auto model_of = [&](int32_t i) { return p->st.req(req_ids[i]).model; };
@@ -821,7 +847,7 @@ cp_status decode_impl(cp_pool *p, int32_t n, const int32_t *req_ids, const void 
         const int32_t v = gk[model_of(i)].variant;
         all_wide = all_wide && is_wide_variant(v);
         any_matrix = any_matrix || v >= kMatrixFirst;
-        pin.push_back(PlanIn{model_of(i), p->st.req(req_ids[i]).ctx_len});
+        pin.push_back(PlanIn{model_of(i), p->st.req(req_ids[i]).attend_len()});
         hb.push_back(hblk[i]);
       }
       std::vector<Geom> geoms;
@@ -894,8 +920,8 @@ cp_status decode_impl(cp_pool *p, int32_t n, const int32_t *req_ids, const void 
     for (int32_t i : g.idx) {
       const Request &r = p->st.req(req_ids[i]);
       DecReq &d = a.req[a.n_req++];
-      d.pte_base = r.pte_base;
-      d.ctx_len = (uint32_t)r.ctx_len;
+      d.pte_base = r.plane_base(r.cursor);  // the KV plane of the request's current layer
+      d.ctx_len = (uint32_t)r.attend_len();
       d.q_off = (uint32_t)q_off[i];
       d.o_off = (uint32_t)o_off[i];
       d.lse_off = (uint32_t)l_off[i];
@@ -979,53 +1005,91 @@ cp_status cp_attn_decode_step(cp_pool *p, int32_t n, const int32_t *req_ids, con
       return fail(CP_EINVAL, "cp_attn_decode_step appends 0 or 1 rows per request (request %d: %d)", req_ids[i],
                   n_new[i]);
     const Request &r = p->st.req(req_ids[i]);
-    if (r.ctx_len + n_new[i] < 1) return fail(CP_EINVAL, "request %d has an empty context", req_ids[i]);
-    if (r.ctx_len + n_new[i] > 0xFFFFFFF0ll) return fail(CP_EINVAL, "context length overflow");
-    if (!p->st.fits_reservation(req_ids[i], r.ctx_len + n_new[i]))
-      return fail(CP_EINVAL, "request %d would grow past its reservation of %lld pages", req_ids[i],
-                  (long long)r.reserve_pages);
+    if (r.cursor == 0) {
+      // the first layer's step may place a new token
+      if (r.ctx_len + n_new[i] < 1) return fail(CP_EINVAL, "request %d has an empty context", req_ids[i]);
+      if (r.ctx_len + n_new[i] > 0xFFFFFFF0ll) return fail(CP_EINVAL, "context length overflow");
+      if (!p->st.fits_reservation(req_ids[i], r.ctx_len + n_new[i]))
+        return fail(CP_EINVAL, "request %d would grow past its reservation of %lld pages", req_ids[i],
+                    (long long)r.reserve_pages);
+    } else if (n_new[i] != r.inflight) {
+      // later layers write the row of the token in flight, if there is one
+      return fail(CP_EINVAL, "request %d is at layer %d of %d %s a token in flight: n_new must be %d", req_ids[i],
+                  r.cursor, r.layers, r.inflight ? "with" : "without", r.inflight);
+    }
     any = any || n_new[i] != 0;
   }
   if (any && !rows) return fail(CP_EINVAL, "null rows");
-  if (!any) return cp_attn_decode_ex(p, n, req_ids, q, out, lse, hip_stream, opts);
+  auto advance_all = [&] {
+    for (int32_t i = 0; i < n; ++i) p->st.advance(req_ids[i]);
+  };
+  if (!any) {
+    rc = cp_attn_decode_ex(p, n, req_ids, q, out, lse, hip_stream, opts);
+    if (rc == CP_OK) advance_all();
+    return rc;
+  }
   uint64_t total_elems = 0;
-  for (int32_t i = 0; i < n; ++i)
-    if (n_new[i]) total_elems += (uint64_t)p->st.model(p->st.req(req_ids[i]).model).row_elems;
-  if (total_elems > 0xFFFFFFFFull) return fail(CP_EINVAL, "too many rows in one call");
-  rc = prepare_growth(p, n, req_ids, n_new);
-  if (rc) return rc;
-
-  // Allocate the new pages on the host; their entries travel with the launch.
-  std::vector<AppendPlan> plan(n);
-  uint64_t off = 0, lo = UINT64_MAX, hi = 0;
+  std::vector<int32_t> placing(n, 0);  // new tokens, placed at the first layer
   for (int32_t i = 0; i < n; ++i) {
     if (!n_new[i]) continue;
     const Request &r = p->st.req(req_ids[i]);
-    const int32_t row_elems = p->st.model(r.model).row_elems;
-    uint64_t first, count;
-    p->st.grow(req_ids[i], r.ctx_len + 1, &first, &count);
+    total_elems += (uint64_t)p->st.model(r.model).row_elems;
+    placing[i] = r.cursor == 0 ? 1 : 0;
+  }
+  if (total_elems > 0xFFFFFFFFull) return fail(CP_EINVAL, "too many rows in one call");
+  rc = prepare_growth(p, n, req_ids, placing.data());
+  if (rc) return rc;
+
+  // Place new tokens (pages of every plane allocated on the host). The
+  // entry of a new page of the current layer's plane travels with the
+  // launch; a multi-layer model's other planes get theirs by one copy.
+  DeviceGuard g(p->device);
+  hipStream_t s = (hipStream_t)hip_stream;
+  const int32_t P = p->st.page_tokens();
+  std::vector<AppendPlan> plan(n);
+  uint64_t off = 0, lo = UINT64_MAX, hi = 0, lo_rest = UINT64_MAX, hi_rest = 0;
+  for (int32_t i = 0; i < n; ++i) {
+    if (!n_new[i]) continue;
+    const Request &r = p->st.req(req_ids[i]);
+    if (placing[i]) {
+      const int64_t used = r.pages_used;
+      uint64_t first, count;
+      p->st.begin_token(req_ids[i], &first, &count);
+      if (count) {
+        lo = std::min(lo, first);
+        hi = std::max(hi, first + count);
+        if (r.layers > 1) {
+          lo_rest = std::min<uint64_t>(lo_rest, r.plane_base(1) + (uint64_t)used);
+          hi_rest = std::max<uint64_t>(hi_rest, r.plane_base(r.layers - 1) + (uint64_t)r.pages_used);
+        }
+      }
+    }
     plan[i].flags = kAppRow;
     plan[i].off = (uint32_t)off;
-    if (count) {
+    if (r.ctx_len % P == 0) {  // the token in flight opens a page
       plan[i].flags |= kAppPage;
-      plan[i].pte = p->st.pte_mirror()[first];
-      lo = std::min(lo, first);
-      hi = std::max(hi, first + count);
+      plan[i].pte = p->st.pte_mirror()[r.plane_base(r.cursor) + (uint64_t)(r.ctx_len / P)];
     }
-    off += (uint64_t)row_elems;
+    off += (uint64_t)p->st.model(r.model).row_elems;
   }
-  rc = decode_impl(p, n, req_ids, q, out, lse, hip_stream, &o, rows, &plan);
+  rc = push_ptes(p, lo_rest, hi_rest, s);
+  if (rc == CP_OK) rc = decode_impl(p, n, req_ids, q, out, lse, hip_stream, &o, rows, &plan);
   if (rc) {
     // keep the device pool in step with the host tables: write the new page
     // entries and rows the unfused way (rewriting a fused row is harmless)
     const std::string msg = cp_last_error();
-    DeviceGuard g(p->device);
-    std::vector<uint32_t> old_len(n);
-    for (int32_t i = 0; i < n; ++i) old_len[i] = (uint32_t)(p->st.req(req_ids[i]).ctx_len - n_new[i]);
-    push_ptes(p, lo, hi, (hipStream_t)hip_stream);
-    launch_appends(p, n, req_ids, n_new, rows, old_len.data(), (hipStream_t)hip_stream);
+    std::vector<AppItem> items;
+    for (int32_t i = 0; i < n; ++i) {
+      if (!n_new[i]) continue;
+      const Request &r = p->st.req(req_ids[i]);
+      items.push_back(AppItem{r.model, 1u, (uint32_t)r.ctx_len, r.plane_base(r.cursor), plan[i].off});
+    }
+    push_ptes(p, std::min(lo, lo_rest), std::max(hi, hi_rest), s);
+    launch_appends(p, items, rows, s);
+    advance_all();
     return fail(rc, "%s", msg.c_str());
   }
+  advance_all();
   return CP_OK;
 }
 

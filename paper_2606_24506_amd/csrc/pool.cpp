@@ -138,6 +138,7 @@ std::string PoolState::add_model(const Geom &gi, int32_t *id) {
   }
   if (g.d_k > 1024) return "K width above 1024";
   if (!(g.d_v == 64 || g.d_v == 128 || g.d_v == 256 || g.d_v == 512)) return "V width must be 64, 128, 256 or 512";
+  if (g.layers < 1 || g.layers > 1024) return "n_layers must be in [1, 1024]";
   g.g = g.hq / g.hkv;
   g.kappa = 2 * g.row_elems;
   if (g.kappa < 128) return "per-token KV bytes below 128";
@@ -177,7 +178,13 @@ int PoolState::open(int32_t model, int64_t reserve_tokens, int32_t *id, std::str
     *err = "reserve_tokens must be >= 1";
     return -1;
   }
-  int64_t pages = ceil_div(reserve_tokens, P_);
+  const int64_t plane = ceil_div(reserve_tokens, P_);
+  const int32_t layers = models_[model].layers;
+  if (plane > (int64_t)pte_.size() / layers) {
+    *err = "reservation larger than the pool";
+    return -3;
+  }
+  int64_t pages = plane * layers;
   if (pages > (int64_t)pte_.size()) {
     *err = "reservation larger than the pool";
     return -3;
@@ -202,8 +209,12 @@ int PoolState::open(int32_t model, int64_t reserve_tokens, int32_t *id, std::str
   r.model = model;
   r.ctx_len = 0;
   r.reserve_pages = pages;
+  r.plane = plane;
   r.pages_used = 0;
   r.pte_base = (uint32_t)base;
+  r.layers = layers;
+  r.cursor = 0;
+  r.inflight = 0;
   acct_[model].reserved += pages;
   ++n_open_;
   *id = rid;
@@ -223,7 +234,8 @@ int PoolState::open(int32_t model, int64_t reserve_tokens, int32_t *id, std::str
 void PoolState::close(int32_t id) {
   Request &r = reqs_[id];
   const int32_t model = r.model;
-  for (int64_t p = 0; p < r.pages_used; ++p) free_page(pte_[r.pte_base + p]);
+  for (int32_t l = 0; l < r.layers; ++l)
+    for (int64_t p = 0; p < r.pages_used; ++p) free_page(pte_[r.plane_base(l) + p]);
   acct_[model].reserved -= r.reserve_pages;
   pte_ranges_.release(r.pte_base, (uint64_t)r.reserve_pages);
   r = Request{};
@@ -234,23 +246,50 @@ void PoolState::close(int32_t id) {
 
 bool PoolState::fits_reservation(int32_t id, int64_t new_len) const {
   const Request &r = reqs_[id];
-  return ceil_div(new_len, P_) <= r.reserve_pages;
+  return ceil_div(new_len, P_) <= r.plane;
+}
+
+// Allocates pages of every plane up to new_len tokens; the entries written
+// lie in [*first, *first + *count) (plane-major, so the range may include
+// unchanged entries between planes).
+static void grow_planes(Request &r, int64_t new_len, uint64_t *first, uint64_t *count,
+                        std::vector<uint32_t> &pte, const std::function<uint32_t()> &alloc, int32_t P) {
+  const int64_t need = (new_len + P - 1) / P;
+  *first = 0;
+  *count = 0;
+  if (need <= r.pages_used) return;
+  for (int32_t l = 0; l < r.layers; ++l)
+    for (int64_t p = r.pages_used; p < need; ++p) pte[r.plane_base(l) + p] = alloc();
+  *first = r.plane_base(0) + (uint64_t)r.pages_used;
+  *count = (uint64_t)(r.plane_base(r.layers - 1) + need) - *first;
+  r.pages_used = need;
 }
 
 void PoolState::grow(int32_t id, int64_t new_len, uint64_t *first, uint64_t *count) {
   Request &r = reqs_[id];
-  int64_t need = ceil_div(new_len, P_);
-  *first = r.pte_base + (uint64_t)r.pages_used;
-  *count = need > r.pages_used ? (uint64_t)(need - r.pages_used) : 0;
-  for (int64_t p = r.pages_used; p < need; ++p) pte_[r.pte_base + p] = alloc_page(r.model);
-  if (need > r.pages_used) r.pages_used = need;
+  grow_planes(r, new_len, first, count, pte_, [&] { return alloc_page(r.model); }, P_);
   r.ctx_len = new_len;
+}
+
+void PoolState::begin_token(int32_t id, uint64_t *first, uint64_t *count) {
+  Request &r = reqs_[id];
+  grow_planes(r, r.ctx_len + 1, first, count, pte_, [&] { return alloc_page(r.model); }, P_);
+  r.inflight = 1;
+}
+
+void PoolState::advance(int32_t id) {
+  Request &r = reqs_[id];
+  if (++r.cursor == r.layers) {
+    r.cursor = 0;
+    r.ctx_len += r.inflight;
+    r.inflight = 0;
+  }
 }
 
 int64_t PoolState::pages_to_grow(int32_t id, int64_t new_len) const {
   const Request &r = reqs_[id];
   int64_t need = ceil_div(new_len, P_);
-  return need > r.pages_used ? need - r.pages_used : 0;
+  return need > r.pages_used ? (need - r.pages_used) * r.layers : 0;
 }
 
 bool PoolState::ensure_slots(int32_t model, int64_t pages, std::vector<int32_t> *carved) {

@@ -40,15 +40,28 @@ struct Geom {
   int64_t page_bytes = 0;
   int32_t ppc = 0;        // pages per chunk
   float scale = 0.f;
+  int32_t layers = 1;     // attention layers: one KV plane (page set) each
 };
 
+// A request of a model with L layers owns L KV planes (Section 3.2: the
+// layer-wise pipeline decodes one layer per stage). Plane l's page-table
+// entries are [pte_base + l * plane, pte_base + l * plane + pages_used);
+// every plane holds the same token positions. A decode step visits one layer:
+// `cursor` is the next layer of the request's token in flight (`inflight`
+// = 1 while the new token has been placed but not yet seen by all layers).
 struct Request {
   bool open = false;
   int32_t model = -1;
-  int64_t ctx_len = 0;
-  int64_t reserve_pages = 0;
-  int64_t pages_used = 0;
+  int64_t ctx_len = 0;        // committed tokens (present in every plane)
+  int64_t reserve_pages = 0;  // all planes
+  int64_t plane = 0;          // page-table entries per plane
+  int64_t pages_used = 0;     // per plane
   uint32_t pte_base = 0;
+  int32_t layers = 1;
+  int32_t cursor = 0;
+  int32_t inflight = 0;
+  int64_t attend_len() const { return ctx_len + inflight; }
+  uint32_t plane_base(int32_t layer) const { return pte_base + (uint32_t)(layer * plane); }
 };
 
 // Deterministic 64-bit generator (splitmix64), used for seeded placement.
@@ -120,12 +133,20 @@ class PoolState {
   // Would growing these requests to the given lengths stay within their
   // reservations? (checked before any state change)
   bool fits_reservation(int32_t id, int64_t new_len) const;
-  // Allocate the pages needed to grow request id to new_len tokens and
-  // record them in the PTE mirror. Returns the index range of PTEs written
-  // as [*first, *first + *count). Never fails for admitted requests within
-  // their reservation.
+  // Allocate the pages needed to grow request id to new_len tokens in every
+  // plane, record them in the PTE mirror, and commit new_len. Returns the
+  // index range covering the PTEs written as [*first, *first + *count).
+  // Never fails for admitted requests within their reservation (after
+  // ensure_slots).
   void grow(int32_t id, int64_t new_len, uint64_t *first, uint64_t *count);
-  // Pages request id still needs to reach new_len tokens.
+  // Places a new token at position ctx_len (pages in every plane as
+  // needed) without committing it: the request's layers then see it one
+  // decode step at a time. Requires cursor 0 and no token in flight.
+  void begin_token(int32_t id, uint64_t *first, uint64_t *count);
+  // After a decode step at the request's cursor: moves to the next layer;
+  // past the last one, commits the token in flight.
+  void advance(int32_t id);
+  // Pages request id still needs (all planes) to reach new_len tokens.
   int64_t pages_to_grow(int32_t id, int64_t new_len) const;
   // Carves fresh chunks for a model until it has at least `pages` free page
   // slots, appending each to *carved. Returns false if a chunk could not be

@@ -393,3 +393,49 @@ def test_random_traffic_invariants_both_backings(backing):
         p.close(r)
     assert p.stats()["chunks_used"] == 0
     p.destroy()
+
+
+# ---------------------------------------------------------------- layer planes
+
+def test_layer_planes_tables_and_budget():
+    chunk = 2 << 20
+    p = host_pool(pool_bytes=8 * chunk, chunk=chunk)
+    a = p.register_spec(MLA16, n_layers=3)
+    info = p.info(a)
+    assert info["n_layers"] == 3
+    ppc = info["pages_per_chunk"]
+    r = p.open(a, ppc * 64)  # one chunk per plane
+    assert p.stats()["pages_reserved"] == 3 * ppc
+    p.append([r], [200], None)
+    t = p.pages(r, layers=3)
+    assert t.shape == (3, 4) and len(set(t.ravel().tolist())) == 12  # distinct pages in every plane
+    assert p.stats()["pages_used"] == 12 and p.ctx_len(r) == 200
+    assert p.cursor(r) == (0, 0)
+    # the budget counts every plane: 3 of 8 chunks reserved, a second
+    # request of two chunks per plane does not fit
+    with pytest.raises(cpl.CrossPoolError) as e:
+        p.open(a, 2 * ppc * 64)
+    assert e.value.status == cpl.CP_ENOSPC
+    r2 = p.open(a, ppc * 64 // 2)
+    with pytest.raises(cpl.CrossPoolError):
+        p.append([r2], [ppc * 64 // 2 + 1], None)  # past the reservation of each plane
+    p.close(r)
+    p.close(r2)
+    assert p.stats()["chunks_used"] == 0 and p.stats()["pages_used"] == 0
+    with pytest.raises(cpl.CrossPoolError, match="n_layers"):
+        p.register_spec(MLA16, n_layers=1025)
+    p.destroy()
+
+
+def test_layer_planes_on_a_virtual_pool_map_every_plane_at_admission():
+    chunk = 2 << 20
+    p = virtual_pool(pool_bytes=16 * chunk, chunk=chunk)
+    a = p.register_spec(MQA32, n_layers=4)
+    ppc = p.info(a)["pages_per_chunk"]
+    r = p.open(a, ppc * 64 + 1)  # two chunks' worth of pages per plane
+    assert p.stats()["chunks_used"] == -(-4 * (ppc + 1) // ppc)
+    p.append([r], [ppc * 64 + 1], None)
+    assert p.stats()["chunks_used"] == -(-4 * (ppc + 1) // ppc)
+    p.close(r)
+    assert p.stats()["chunks_used"] == 0
+    p.destroy()
