@@ -58,6 +58,9 @@ def parse():
                     help="step as cp_kv_append + cp_attn_decode_ex instead of cp_attn_decode_step")
     ap.add_argument("--backing", type=int, default=0, choices=[0, 1],
                     help="pool memory: 0 one device buffer, 1 virtual ranges with chunks mapped on demand")
+    ap.add_argument("--planes", action="store_true",
+                    help="one pool whose models have one KV plane per layer, the steps moving each request's "
+                         "layer cursor, instead of one pool per layer")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="target CPU time of the oracle sample")
     ap.add_argument("--copy-mib", type=int, default=0,
@@ -184,8 +187,16 @@ def main():
 
     rows_cache = {r: wl.rows_bits(r) for r in range(len(wl.requests))}
     inter = 512 if args.config == 4 else (4096 if args.config == 5 else 0)
-    lds = [load(wl, reserve_extra=grow, interleave=inter, rows_override=rows_cache,
-                placement_seed=wl.placement_seed + 1000 * i, backing=args.backing) for i in range(layers)]
+    if args.planes:
+        if wl.filler_pages:
+            sys.exit("--planes: the filler requests of this pool leave no room for more than one KV plane")
+        # one pool, L planes: step i serves layer i % L of every request
+        one = load(wl, reserve_extra=grow, interleave=inter, rows_override=rows_cache,
+                   placement_seed=wl.placement_seed, backing=args.backing, n_layers=layers)
+        lds = [one] * layers
+    else:
+        lds = [load(wl, reserve_extra=grow, interleave=inter, rows_override=rows_cache,
+                    placement_seed=wl.placement_seed + 1000 * i, backing=args.backing) for i in range(layers)]
     del rows_cache
     B = len(wl.requests)
     # one new token per request per step: seeded rows, resident on the GPU before timing
@@ -234,6 +245,9 @@ def main():
         n_warm += max(0, more)
         torch.cuda.synchronize()
     ctx0 = [[ld.pool.ctx_len(r) for r in ld.req_ids] for ld in lds]
+    if args.planes:  # tokens in flight through the planes count for the layers they reached
+        ctx0 = [[c + (li < lds[0].pool.cursor(r)[0]) for c, r in zip(ctx0[li], lds[0].req_ids)]
+                for li in range(layers)]
     # Throughput pass: K steps with nothing but the work in the stream.
     t0 = time.perf_counter()
     for i in range(args.steps):
@@ -292,6 +306,7 @@ def main():
             "path": ["auto", "vector", "matrix"][args.path],
             "schedule": ["balanced", "queue", "grid"][args.schedule],
             "backing": ["buffer", "virtual"][args.backing],
+            "layers_as": "KV planes of one pool (layer cursor)" if args.planes else "one pool per layer",
         },
         "req_tokens_per_s": round(B / (wall / args.steps), 1),
         "host_enqueue_ms_per_step": round(t_enq * 1e3 / args.steps, 5),
@@ -319,7 +334,7 @@ def main():
     }
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
-    for ld in lds:
+    for ld in (lds[:1] if args.planes else lds):
         ld.close()
     print(json.dumps(res))
 

@@ -57,13 +57,16 @@ def to_device_u16(arr: np.ndarray, device):
 
 def load(wl: Workload, device: int = 0, *, placement_seed: Optional[int] = None, reserve_extra: int = 0,
          interleave: int = 0, rows_override: Optional[Dict[int, np.ndarray]] = None,
-         q_override: Optional[List[np.ndarray]] = None, chunk_rows: int = 1 << 17, backing: int = 0) -> Loaded:
+         q_override: Optional[List[np.ndarray]] = None, chunk_rows: int = 1 << 17, backing: int = 0,
+         n_layers: int = 1) -> Loaded:
     """Build a pool holding the workload.
 
     interleave > 0 appends rows in rounds of `interleave` tokens per request,
     so physical pages of different requests alternate. rows_override maps a
     request index to its rows (uint16 bits) instead of the seeded draw.
     backing selects the pool's memory (0 one buffer, 1 virtual ranges).
+    n_layers > 1 registers the models with that many KV planes, each holding
+    the same rows.
     """
     import torch
 
@@ -73,9 +76,9 @@ def load(wl: Workload, device: int = 0, *, placement_seed: Optional[int] = None,
     seed = wl.placement_seed if placement_seed is None else placement_seed
     pool = cpl.Pool(page_tokens=PAGE_TOKENS, pool_bytes=wl.pool_bytes, chunk_bytes=wl.chunk_bytes,
                     placement_seed=seed, device=device, backing=backing)
-    mids = {name: pool.register_spec(MODELS[name]) for name in wl.models_used()}
+    mids = {name: pool.register_spec(MODELS[name], n_layers=n_layers) for name in wl.models_used()}
     if wl.filler_model and wl.filler_model not in mids:
-        mids[wl.filler_model] = pool.register_spec(MODELS[wl.filler_model])
+        mids[wl.filler_model] = pool.register_spec(MODELS[wl.filler_model], n_layers=n_layers)
     rids = [pool.open(mids[rq.model], rq.ctx_len + reserve_extra) for rq in wl.requests]
 
     # Filler requests occupy pool pages around the batch (their content is
@@ -90,7 +93,8 @@ def load(wl: Workload, device: int = 0, *, placement_seed: Optional[int] = None,
         left -= take
     filler_page = None
     if fillers:
-        filler_page = torch.zeros((PAGE_TOKENS, MODELS[wl.filler_model].row_width), dtype=torch.int16, device=dev)
+        filler_page = torch.zeros((n_layers, PAGE_TOKENS, MODELS[wl.filler_model].row_width), dtype=torch.int16,
+                                  device=dev)
 
     def rows_of(r):
         if rows_override and r in rows_override:
@@ -101,8 +105,9 @@ def load(wl: Workload, device: int = 0, *, placement_seed: Optional[int] = None,
         for r, rid in enumerate(rids):
             rows = rows_of(r)
             for s in range(0, rows.shape[0], chunk_rows):
-                blk = to_device_u16(rows[s:s + chunk_rows], dev)
-                pool.append([rid], [blk.shape[0]], blk)
+                part = rows[s:s + chunk_rows]
+                blk = to_device_u16(np.tile(part.reshape(-1), n_layers), dev)  # [layers][tokens][row]
+                pool.append([rid], [part.shape[0]], blk)
             torch.cuda.synchronize(dev)
         for f, cap in zip(fillers, fcap):
             for _ in range(cap):
@@ -119,7 +124,7 @@ def load(wl: Workload, device: int = 0, *, placement_seed: Optional[int] = None,
                 if k > 0:
                     ids.append(rid)
                     nn.append(k)
-                    blocks.append(all_rows[r][pos[r]:pos[r] + k].reshape(-1))
+                    blocks.append(np.tile(all_rows[r][pos[r]:pos[r] + k].reshape(-1), n_layers))
                     pos[r] += k
             if ids:
                 pool.append(ids, nn, to_device_u16(np.concatenate(blocks), dev))
