@@ -977,8 +977,8 @@ cp_status decode_impl(cp_pool *p, int32_t n, const int32_t *req_ids, const void 
     m.ws_orow = ws_orow[i];
     m.o_off = (uint32_t)o_off[i];
     m.lse_off = (uint32_t)l_off[i];
-    // one workgroup per (head, block of 128 V columns)
-    ma.n_blocks += g.hq * std::max(1, g.d_v / 128);
+    // one workgroup per (head, block of V columns)
+    ma.n_blocks += g.hq * (int32_t)((uint32_t)g.d_v / merge_block_cols((uint32_t)g.d_v));
   }
   return flush();
 }

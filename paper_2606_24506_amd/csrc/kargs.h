@@ -93,6 +93,10 @@ struct DecodeArgs {
   DecReq req[kMaxReqPerLaunch];
 };
 
+// V columns one merge workgroup covers: 64 lanes of up to four columns
+// (d_v is 64, 128, 256 or 512).
+constexpr uint32_t merge_block_cols(uint32_t d_v) { return d_v >= 256 ? 256u : d_v; }
+
 struct MergeReq {
   uint32_t block_begin;  // first merge workgroup of this request
   uint32_t hq, d_v, n_chunks;

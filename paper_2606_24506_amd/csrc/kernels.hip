@@ -10,6 +10,8 @@
 #include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
+#include <type_traits>
+
 #include "decode_mfma.h"
 #include "decode_narrow.h"
 #include "decode_small.h"
@@ -424,94 +426,138 @@ int decode_wgs_per_cu(uint32_t mask) {
 
 // ------------------------------------------------------------- merge
 
-// Split merge. One workgroup per (split request, query head, block of 128
-// V columns). First every thread takes some partials' lse values and the
-// block finds M = max_c lse_c; then wave w folds partials c = w, w+4, ...
-// with weights exp(lse_c - M) into its accumulators, and the four wave sums
-// are added in wave order:
+// Split merge. One workgroup per (split request, query head, block of
+// merge_block_cols(d_v) V columns); lane i of every wave covers PER
+// consecutive columns of the block. First every thread takes some partials'
+// lse values and the block finds M = max_c lse_c; then wave w of the NW
+// waves folds partials c = w, w + NW, ... with weights exp(lse_c - M) into
+// its accumulators, up to kMergeUnroll partials' loads in flight at a time,
+// and the wave sums are added in wave order:
 //   lse = M + ln sum_c exp(lse_c - M),  o = sum_c exp(lse_c - lse) o_c.
-__global__ __launch_bounds__(256) void merge_kernel(const MergeArgs a) {
-  __shared__ float red[4];
-  __shared__ float part[3][128];
-  const uint32_t nblk_total = blockIdx.x;
-  const int r = sorted_search(a.n_req, nblk_total, [&](int i) { return a.req[i].block_begin; });
-  const MergeReq &rq = a.req[r];
-  const uint32_t dblocks = rq.d_v / 128 ? rq.d_v / 128 : 1;
-  const uint32_t local = nblk_total - rq.block_begin;
-  const uint32_t h = local / dblocks, db = local % dblocks;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+// The partials were written by the decode launch just before, so they are
+// mostly read back from the Infinity Cache; the kernel is bound by how many
+// loads it keeps in flight, hence whole 8-byte column groups per lane and,
+// for many partials, eight waves (NW is the launch's workgroup size / 64).
+constexpr int kMergeMaxWaves = 8, kMergeUnroll = 8;
+
+template <int PER>
+__device__ __forceinline__ void merge_block(const MergeArgs &a, const MergeReq &rq, uint32_t h, uint32_t db, float M,
+                                            float (*part)[256], float *red) {
   constexpr float kLog2e = 1.4426950408889634f;
-  const uint32_t n = rq.n_chunks;
-  const uint64_t lrow0 = (uint64_t)rq.ws_base + h;  // lse of chunk c at lrow0 + c * hq
-  // block maximum of the partial lse values (log2 domain)
-  float mx = -INFINITY;
-  for (uint32_t c = threadIdx.x; c < n; c += 256) mx = fmaxf(mx, a.ws_l[lrow0 + (uint64_t)c * rq.hq] * kLog2e);
-  mx = wave_max(mx);
-  if (lane == 0) red[wave] = mx;
-  __syncthreads();
-  const float M = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
-  __syncthreads();
-  // weighted sums; this lane covers columns db*128 + 2*lane (+1) when d_v >= 128
-  const uint32_t dv = rq.d_v;
-  const uint32_t per = dv >= 128 ? 2 : dv / 64;  // floats per lane
-  const uint32_t d0 = db * 128 + lane * per;
-  float acc0 = 0.f, acc1 = 0.f, l = 0.f;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const uint32_t nw = blockDim.x >> 6;
+  const uint32_t dv = rq.d_v, n = rq.n_chunks;
+  const uint32_t d0 = db * (64 * PER) + lane * PER;
+  const uint64_t lrow0 = (uint64_t)rq.ws_base + h;
   const uint16_t *obase = a.ws_o + ((uint64_t)rq.ws_orow + h) * dv + d0;
   const uint64_t ostride = (uint64_t)rq.hq * dv;
-  uint32_t c = wave;
-  for (; c + 12 < n; c += 16) {
-    float w[4], x0[4], x1[4];
+  float acc[PER], l = 0.f;
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const uint32_t cc = c + 4 * u;
-      w[u] = a.ws_l[lrow0 + (uint64_t)cc * rq.hq];
-      const uint16_t *src = obase + (uint64_t)cc * ostride;
-      x0[u] = bf16_to_f32(src[0]);
-      x1[u] = per > 1 ? bf16_to_f32(src[1]) : 0.f;
+  for (int j = 0; j < PER; ++j) acc[j] = 0.f;
+  // batches of kMergeUnroll partials; only the last may be partial (its
+  // test is uniform per wave)
+  auto batch = [&](uint32_t c, auto full) {
+    float w[kMergeUnroll], x[kMergeUnroll][PER];
+#pragma unroll
+    for (int u = 0; u < kMergeUnroll; ++u) {
+      const uint32_t cc = c + nw * u;
+      w[u] = -INFINITY;
+#pragma unroll
+      for (int j = 0; j < PER; ++j) x[u][j] = 0.f;
+      if (decltype(full)::value || cc < n) {
+        w[u] = a.ws_l[lrow0 + (uint64_t)cc * rq.hq] * kLog2e - M;
+        const uint16_t *src = obase + (uint64_t)cc * ostride;
+        if constexpr (PER == 4) {
+          const uint2 v = *reinterpret_cast<const uint2 *>(src);
+          x[u][0] = bf16_to_f32(v.x);
+          x[u][1] = bf16_to_f32(v.x >> 16);
+          x[u][2] = bf16_to_f32(v.y);
+          x[u][3] = bf16_to_f32(v.y >> 16);
+        } else if constexpr (PER == 2) {
+          const uint32_t v = *reinterpret_cast<const uint32_t *>(src);
+          x[u][0] = bf16_to_f32(v);
+          x[u][1] = bf16_to_f32(v >> 16);
+        } else {
+          x[u][0] = bf16_to_f32(src[0]);
+        }
+      }
     }
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const float wu = fast_exp2(w[u] * kLog2e - M);
+    for (int u = 0; u < kMergeUnroll; ++u) {
+      const float wu = fast_exp2(w[u]);  // 0 for the partials past n
       l += wu;
-      acc0 = fmaf(wu, x0[u], acc0);
-      acc1 = fmaf(wu, x1[u], acc1);
+#pragma unroll
+      for (int j = 0; j < PER; ++j) acc[j] = fmaf(wu, x[u][j], acc[j]);
     }
-  }
-  for (; c < n; c += 4) {
-    const float wu = fast_exp2(a.ws_l[lrow0 + (uint64_t)c * rq.hq] * kLog2e - M);
-    const uint16_t *src = obase + (uint64_t)c * ostride;
-    l += wu;
-    acc0 = fmaf(wu, bf16_to_f32(src[0]), acc0);
-    if (per > 1) acc1 = fmaf(wu, bf16_to_f32(src[1]), acc1);
-  }
-  // combine the four waves in order
+  };
+  uint32_t c = wave;
+  for (; c + nw * (kMergeUnroll - 1) < n; c += nw * kMergeUnroll) batch(c, std::true_type{});
+  if (c < n) batch(c, std::false_type{});
+  // combine the waves in order
   if (wave > 0) {
-    part[wave - 1][2 * lane] = acc0;
-    part[wave - 1][2 * lane + 1] = acc1;
+#pragma unroll
+    for (int j = 0; j < PER; ++j) part[wave - 1][PER * lane + j] = acc[j];
     if (lane == 0) red[wave] = l;
   }
   __syncthreads();
   if (wave == 0) {
     float L = l;
+    for (uint32_t w2 = 1; w2 < nw; ++w2) {
 #pragma unroll
-    for (int w2 = 1; w2 < 4; ++w2) {
-      acc0 += part[w2 - 1][2 * lane];
-      acc1 += part[w2 - 1][2 * lane + 1];
+      for (int j = 0; j < PER; ++j) acc[j] += part[w2 - 1][PER * lane + j];
       L += red[w2];
     }
     const float inv = 1.0f / L;
-    if (d0 < dv) {
-      uint16_t *dst = a.out + rq.o_off + h * dv + d0;
-      dst[0] = (uint16_t)f32_to_bf16(acc0 * inv);
-      if (per > 1) dst[1] = (uint16_t)f32_to_bf16(acc1 * inv);
+    uint16_t *dst = a.out + rq.o_off + h * dv + d0;
+    if constexpr (PER == 4) {
+      *reinterpret_cast<uint2 *>(dst) = bf16x4_bits(acc[0] * inv, acc[1] * inv, acc[2] * inv, acc[3] * inv);
+    } else {
+#pragma unroll
+      for (int j = 0; j < PER; ++j) dst[j] = (uint16_t)f32_to_bf16(acc[j] * inv);
     }
     if (lane == 0 && db == 0) a.lse[rq.lse_off + h] = (M + fast_log2(L)) * kLn2;
   }
 }
 
+__global__ __launch_bounds__(64 * kMergeMaxWaves) void merge_kernel(const MergeArgs a) {
+  __shared__ float red[kMergeMaxWaves];
+  __shared__ float part[kMergeMaxWaves - 1][256];
+  const uint32_t nblk_total = blockIdx.x;
+  const int r = sorted_search(a.n_req, nblk_total, [&](int i) { return a.req[i].block_begin; });
+  const MergeReq &rq = a.req[r];
+  const uint32_t dblocks = rq.d_v / merge_block_cols(rq.d_v);
+  const uint32_t local = nblk_total - rq.block_begin;
+  const uint32_t h = local / dblocks, db = local % dblocks;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const uint32_t nw = blockDim.x >> 6;
+  constexpr float kLog2e = 1.4426950408889634f;
+  const uint32_t n = rq.n_chunks;
+  const uint64_t lrow0 = (uint64_t)rq.ws_base + h;  // lse of chunk c at lrow0 + c * hq
+  // block maximum of the partial lse values (log2 domain)
+  float mx = -INFINITY;
+  for (uint32_t c = threadIdx.x; c < n; c += blockDim.x) mx = fmaxf(mx, a.ws_l[lrow0 + (uint64_t)c * rq.hq] * kLog2e);
+  mx = wave_max(mx);
+  if (lane == 0) red[wave] = mx;
+  __syncthreads();
+  float M = red[0];
+  for (uint32_t w = 1; w < nw; ++w) M = fmaxf(M, red[w]);
+  __syncthreads();
+  const uint32_t per = merge_block_cols(rq.d_v) / 64;
+  if (per == 4)
+    merge_block<4>(a, rq, h, db, M, part, red);
+  else if (per == 2)
+    merge_block<2>(a, rq, h, db, M, part, red);
+  else
+    merge_block<1>(a, rq, h, db, M, part, red);
+}
+
 hipError_t launch_merge(const MergeArgs &a, hipStream_t stream) {
   if (a.n_blocks <= 0) return hipSuccess;
-  hipLaunchKernelGGL(merge_kernel, dim3(a.n_blocks), dim3(256), 0, stream, a);
+  // eight waves when some request has many partials, four otherwise
+  int max_n = 0;
+  for (int i = 0; i < a.n_req; ++i) max_n = a.req[i].n_chunks > (uint32_t)max_n ? (int)a.req[i].n_chunks : max_n;
+  const int waves = max_n >= 8 * kMergeUnroll ? kMergeMaxWaves : 4;
+  hipLaunchKernelGGL(merge_kernel, dim3(a.n_blocks), dim3(64 * waves), 0, stream, a);
   return hipGetLastError();
 }
 
