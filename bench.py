@@ -86,20 +86,22 @@ def kernel_source_hash() -> str:
 
 
 def measured_traffic(cfg: int):
-    """HBM bytes of one decode launch from the committed rocprofv3 counter
-    summary of this workload (scaled FETCH_SIZE + WRITE_SIZE), or None when
-    there is none or the kernel sources changed since it was taken."""
+    """(HBM bytes, algorithmic bytes) of one decode launch from the committed
+    rocprofv3 counter summary of this workload (scaled FETCH_SIZE +
+    WRITE_SIZE, and the algorithmic bytes of the counted launches, whose
+    contexts are close to but not exactly those of this run), or (None,
+    None) when there is none or the kernel sources changed since."""
     path = os.path.join(ROOT, "profiles", PROFILE_NAMES.get(cfg, "") + ".json")
     if not os.path.exists(path):
-        return None
+        return None, None
     try:
         d = json.load(open(path))
         if d.get("kernel_source_sha256") != kernel_source_hash() or d.get("workload_config") != cfg:
-            return None
+            return None, None
         k = d["decode_kernel"]
-        return float(k["read_bytes"] + k["write_bytes"])
+        return float(k["read_bytes"] + k["write_bytes"]), k.get("algorithmic_bytes_per_launch")
     except (OSError, ValueError, KeyError):
-        return None
+        return None, None
 
 
 def algorithmic_bytes_decode(wl, ctx):
@@ -282,6 +284,7 @@ def main():
     ms_per_step = wall * 1e3 / args.steps
     achieved = dec_bytes_timed / args.steps / (kern_ms * 1e-3) / 1e9
     tflops = dec_flops_timed / args.steps / (kern_ms * 1e-3) / 1e12
+    traffic, traffic_alg = measured_traffic(args.config)
     res = {
         "metric": "paged decode-attention achieved HBM GB/s and req-tokens/s on 1 MI355X",
         "value": round(value, 2),
@@ -318,8 +321,9 @@ def main():
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBS, 4),
-            "traffic": measured_traffic(args.config),
+            "traffic": traffic,
             "traffic_unit": "bytes per decode launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
+            "traffic_algorithmic_bytes": traffic_alg,  # of the launches the counters saw
             "algorithmic_bytes_per_launch": int(dec_bytes_timed / args.steps),
             "kernel_ms": round(kern_ms, 5),
         },
