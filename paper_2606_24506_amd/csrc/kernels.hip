@@ -428,34 +428,35 @@ int decode_wgs_per_cu(uint32_t mask) {
 
 // Split merge. One workgroup per (split request, query head, block of
 // merge_block_cols(d_v) V columns); lane i of every wave covers PER
-// consecutive columns of the block. First every thread takes some partials'
-// lse values and the block finds M = max_c lse_c; then wave w of the NW
-// waves folds partials c = w, w + NW, ... with weights exp(lse_c - M) into
-// its accumulators, up to kMergeUnroll partials' loads in flight at a time,
-// and the wave sums are added in wave order:
+// consecutive columns of the block. Wave w of the NW waves folds partials
+// c = w, w + NW, ... in batches of kMergeUnroll, each batch's lse values and
+// outputs loaded together, keeping its own running maximum m_w (log2 domain)
+// and rescaling its sums when a batch raises it. The waves then combine in
+// wave order with M = max_w m_w:
 //   lse = M + ln sum_c exp(lse_c - M),  o = sum_c exp(lse_c - lse) o_c.
-// The partials were written by the decode launch just before, so they are
-// mostly read back from the Infinity Cache; the kernel is bound by how many
-// loads it keeps in flight, hence whole 8-byte column groups per lane and,
-// for many partials, eight waves (NW is the launch's workgroup size / 64).
+// One pass over the partials, so one round trip to memory per batch. The
+// partials were written by the decode launch just before and mostly come
+// back from the Infinity Cache; the kernel is bound by how many loads it
+// keeps in flight, hence whole 8-byte column groups per lane and, for many
+// partials, eight waves (NW is the launch's workgroup size / 64).
 constexpr int kMergeMaxWaves = 8, kMergeUnroll = 8;
 
 template <int PER>
-__device__ __forceinline__ void merge_block(const MergeArgs &a, const MergeReq &rq, uint32_t h, uint32_t db, float M,
-                                            float (*part)[256], float *red) {
+__device__ __forceinline__ void merge_block(const MergeArgs &a, const MergeReq &rq, uint32_t h, uint32_t db,
+                                            float (*part)[256], float *red_m, float *red_l) {
   constexpr float kLog2e = 1.4426950408889634f;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const uint32_t nw = blockDim.x >> 6;
   const uint32_t dv = rq.d_v, n = rq.n_chunks;
   const uint32_t d0 = db * (64 * PER) + lane * PER;
-  const uint64_t lrow0 = (uint64_t)rq.ws_base + h;
+  const uint64_t lrow0 = (uint64_t)rq.ws_base + h;  // lse of chunk c at lrow0 + c * hq
   const uint16_t *obase = a.ws_o + ((uint64_t)rq.ws_orow + h) * dv + d0;
   const uint64_t ostride = (uint64_t)rq.hq * dv;
-  float acc[PER], l = 0.f;
+  float acc[PER], l = 0.f, m = -INFINITY;
 #pragma unroll
   for (int j = 0; j < PER; ++j) acc[j] = 0.f;
   // batches of kMergeUnroll partials; only the last may be partial (its
-  // test is uniform per wave)
+  // test is uniform per wave, and its first partial always exists)
   auto batch = [&](uint32_t c, auto full) {
     float w[kMergeUnroll], x[kMergeUnroll][PER];
 #pragma unroll
@@ -465,7 +466,7 @@ __device__ __forceinline__ void merge_block(const MergeArgs &a, const MergeReq &
 #pragma unroll
       for (int j = 0; j < PER; ++j) x[u][j] = 0.f;
       if (decltype(full)::value || cc < n) {
-        w[u] = a.ws_l[lrow0 + (uint64_t)cc * rq.hq] * kLog2e - M;
+        w[u] = a.ws_l[lrow0 + (uint64_t)cc * rq.hq] * kLog2e;
         const uint16_t *src = obase + (uint64_t)cc * ostride;
         if constexpr (PER == 4) {
           const uint2 v = *reinterpret_cast<const uint2 *>(src);
@@ -482,9 +483,19 @@ __device__ __forceinline__ void merge_block(const MergeArgs &a, const MergeReq &
         }
       }
     }
+    float bm = w[0];
+#pragma unroll
+    for (int u = 1; u < kMergeUnroll; ++u) bm = fmaxf(bm, w[u]);
+    if (bm > m) {  // uniform: every lane holds the same lse values
+      const float f = fast_exp2(m - bm);  // 0 on the first batch
+      l *= f;
+#pragma unroll
+      for (int j = 0; j < PER; ++j) acc[j] *= f;
+      m = bm;
+    }
 #pragma unroll
     for (int u = 0; u < kMergeUnroll; ++u) {
-      const float wu = fast_exp2(w[u]);  // 0 for the partials past n
+      const float wu = fast_exp2(w[u] - m);  // 0 for the partials past n
       l += wu;
 #pragma unroll
       for (int j = 0; j < PER; ++j) acc[j] = fmaf(wu, x[u][j], acc[j]);
@@ -493,19 +504,26 @@ __device__ __forceinline__ void merge_block(const MergeArgs &a, const MergeReq &
   uint32_t c = wave;
   for (; c + nw * (kMergeUnroll - 1) < n; c += nw * kMergeUnroll) batch(c, std::true_type{});
   if (c < n) batch(c, std::false_type{});
-  // combine the waves in order
+  // combine the waves in order, each rescaled to the block maximum
+  if (lane == 0) red_m[wave] = m;
+  __syncthreads();
+  float M = red_m[0];
+  for (uint32_t w2 = 1; w2 < nw; ++w2) M = fmaxf(M, red_m[w2]);
+  const float f = m == -INFINITY ? 0.f : fast_exp2(m - M);  // waves without partials add nothing
   if (wave > 0) {
 #pragma unroll
-    for (int j = 0; j < PER; ++j) part[wave - 1][PER * lane + j] = acc[j];
-    if (lane == 0) red[wave] = l;
+    for (int j = 0; j < PER; ++j) part[wave - 1][PER * lane + j] = acc[j] * f;
+    if (lane == 0) red_l[wave] = l * f;
   }
   __syncthreads();
   if (wave == 0) {
-    float L = l;
+    float L = l * f;
+#pragma unroll
+    for (int j = 0; j < PER; ++j) acc[j] *= f;
     for (uint32_t w2 = 1; w2 < nw; ++w2) {
 #pragma unroll
       for (int j = 0; j < PER; ++j) acc[j] += part[w2 - 1][PER * lane + j];
-      L += red[w2];
+      L += red_l[w2];
     }
     const float inv = 1.0f / L;
     uint16_t *dst = a.out + rq.o_off + h * dv + d0;
@@ -520,7 +538,7 @@ __device__ __forceinline__ void merge_block(const MergeArgs &a, const MergeReq &
 }
 
 __global__ __launch_bounds__(64 * kMergeMaxWaves) void merge_kernel(const MergeArgs a) {
-  __shared__ float red[kMergeMaxWaves];
+  __shared__ float red_m[kMergeMaxWaves], red_l[kMergeMaxWaves];
   __shared__ float part[kMergeMaxWaves - 1][256];
   const uint32_t nblk_total = blockIdx.x;
   const int r = sorted_search(a.n_req, nblk_total, [&](int i) { return a.req[i].block_begin; });
@@ -528,27 +546,13 @@ __global__ __launch_bounds__(64 * kMergeMaxWaves) void merge_kernel(const MergeA
   const uint32_t dblocks = rq.d_v / merge_block_cols(rq.d_v);
   const uint32_t local = nblk_total - rq.block_begin;
   const uint32_t h = local / dblocks, db = local % dblocks;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const uint32_t nw = blockDim.x >> 6;
-  constexpr float kLog2e = 1.4426950408889634f;
-  const uint32_t n = rq.n_chunks;
-  const uint64_t lrow0 = (uint64_t)rq.ws_base + h;  // lse of chunk c at lrow0 + c * hq
-  // block maximum of the partial lse values (log2 domain)
-  float mx = -INFINITY;
-  for (uint32_t c = threadIdx.x; c < n; c += blockDim.x) mx = fmaxf(mx, a.ws_l[lrow0 + (uint64_t)c * rq.hq] * kLog2e);
-  mx = wave_max(mx);
-  if (lane == 0) red[wave] = mx;
-  __syncthreads();
-  float M = red[0];
-  for (uint32_t w = 1; w < nw; ++w) M = fmaxf(M, red[w]);
-  __syncthreads();
   const uint32_t per = merge_block_cols(rq.d_v) / 64;
   if (per == 4)
-    merge_block<4>(a, rq, h, db, M, part, red);
+    merge_block<4>(a, rq, h, db, part, red_m, red_l);
   else if (per == 2)
-    merge_block<2>(a, rq, h, db, M, part, red);
+    merge_block<2>(a, rq, h, db, part, red_m, red_l);
   else
-    merge_block<1>(a, rq, h, db, M, part, red);
+    merge_block<1>(a, rq, h, db, part, red_m, red_l);
 }
 
 hipError_t launch_merge(const MergeArgs &a, hipStream_t stream) {
