@@ -152,6 +152,25 @@ def test_every_kernel_variant(schedule, splits):
         ld.close()
 
 
+@pytest.mark.parametrize("schedule,splits", [(BAL, 0), (QUE, 0), (GRD, 2)])
+def test_many_requests_in_one_call(schedule, splits):
+    """150 requests of six models in one call: more requests than one launch
+    takes (64) and more models than one launch holds (4), so the call runs
+    several launch groups and several merge launches."""
+    rng = np.random.default_rng(77)
+    names = ["mla16", "mqa32", "gqa32x4", "gqa16x4d64", "mla128", "mqa128"]
+    lens = [(names[int(rng.integers(0, len(names)))], int(np.exp(rng.uniform(0, np.log(2000))))) for _ in range(150)]
+    wl = custom(lens, seed=78, pool_bytes=1 << 30)
+    print(f"[case] 150 requests sched{schedule} s{splits}", flush=True)
+    ld = load(wl, interleave=50)
+    try:
+        ld.decode(num_splits=splits, schedule=schedule)
+        torch.cuda.synchronize()
+        compare(ld, {r: expected_for(wl, r) for r in range(len(lens))}, f"150 requests sched{schedule}")
+    finally:
+        ld.close()
+
+
 def test_forced_matrix_path_rejects_narrow_groups():
     """One query head per KV head has no matrix-core variant."""
     wl = custom([("gqa8x8d64", 10)], seed=3)
