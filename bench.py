@@ -265,7 +265,9 @@ def main():
     for i in range(args.steps):
         step(n_warm + args.steps + i, ev[i])
     torch.cuda.synchronize()
-    kern_ms = sum(a.elapsed_time(b) for a, b in ev) / args.steps
+    kern_each = sorted(a.elapsed_time(b) for a, b in ev)
+    kern_ms = sum(kern_each) / args.steps
+    pct = lambda q: kern_each[min(len(kern_each) - 1, int(q * len(kern_each)))]
     # algorithmic bytes of the two timed passes (contexts grow by one per visit)
     dec_bytes, app_bytes, dec_bytes_timed, dec_flops_timed = 0, 0, 0, 0
     visits = [0] * layers
@@ -326,6 +328,7 @@ def main():
             "traffic_algorithmic_bytes": traffic_alg,  # of the launches the counters saw
             "algorithmic_bytes_per_launch": int(dec_bytes_timed / args.steps),
             "kernel_ms": round(kern_ms, 5),
+            "kernel_ms_p10_p50_p90": [round(pct(0.1), 5), round(pct(0.5), 5), round(pct(0.9), 5)],
         },
         # the same kernel's attention arithmetic against the dense bf16
         # matrix-core peak (the many-head MLA batches are the ones near it)
