@@ -21,8 +21,11 @@
  *     throws. cp_last_error() gives a thread-local message for the last
  *     failure on the calling thread.
  *   - All argument and capacity checks run on the host before anything is
- *     enqueued; on any error no pool state changes (all-or-nothing across a
- *     whole batch).
+ *     enqueued; on any error they report, no pool state changes
+ *     (all-or-nothing across a whole batch). A HIP failure after the checks
+ *     (CP_EHIP from a copy or launch of an append or decode step) leaves
+ *     the host tables updated as if the call had succeeded; the device
+ *     state is then undefined and the pool should be closed.
  *   - Device-memory arguments are device pointers on the pool's device;
  *     host arguments are ordinary host pointers and are not retained after
  *     the call returns. Streams are hipStream_t passed as void* (NULL = the
