@@ -8,11 +8,18 @@ its own copy of the batch's KV in its own pool, so that consecutive steps
 never find their KV in the 256 MiB Infinity Cache, as when a model's layers
 are decoded one after another.
 
+The headline line measures the DeepSeek-V3-shaped batch (8 requests of 128K
+tokens at 128 query heads), the largest single-GPU workload; the same run
+also measures the V2-Lite-shaped, mixed-model and 512K-burst batches and
+reports each under "per_config". Requests are loaded one token short of
+their configured context (and short by the warmup's appends), so the first
+timed step of every layer attends over exactly the configured lengths.
+
 Prints one JSON line. value = algorithmic bytes moved per second over the
 timed steps (KV read once, queries, outputs, lse, page-table entries, and
 the appended rows read and written), in GB/s.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 2]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 3] [--also 2,4,5]
 """
 from __future__ import annotations
 
@@ -28,10 +35,13 @@ import numpy as np
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
-MAX_AUTO_WARMUP = 4000  # cap of the time-based warmup (sets the tokens reserved for growth)
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E
 MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 matrix-core peak
+MAX_SETTLE_CALLS = 4000
 PROFILE_NAMES = {2: "decode_v2lite_mla16", 3: "decode_v3_mla128", 4: "decode_mixed", 5: "decode_burst_mla128"}
+KERNEL_NAMES = {2: "cp::decode_kernel (narrow matrix MLA-16)", 3: "cp::decode_mla_kernel (MLA-128)",
+                4: "cp::decode_kernel (narrow matrix MLA-16 / MQA-32 / GQA-32:4)",
+                5: "cp::decode_mla_kernel (MLA-128)"}
 WORKLOAD_NAMES = {
     1: "tiny MLA-16 decode: 4 requests {128,256,384,512} tokens, 64-page pool",
     2: "DeepSeek-V2-Lite-shaped MLA-16 decode: 32 requests, log-uniform 1K-32K tokens, 2 GiB pool",
@@ -44,12 +54,15 @@ WORKLOAD_NAMES = {
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=200)
-    ap.add_argument("--warmup", type=int, default=-1,
-                    help="untimed warmup steps (default: as many as fill --warmup-seconds of GPU time)")
-    ap.add_argument("--warmup-seconds", type=float, default=0.3,
-                    help="GPU time the default warmup lasts: clocks and power settle within it")
-    ap.add_argument("--config", type=int, default=2, choices=[1, 2, 3, 4, 5])
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=20, help="untimed warmup steps (each appends a token)")
+    ap.add_argument("--settle-seconds", type=float, default=0.3,
+                    help="GPU time of decode-only calls (no appends) run before the warmup steps, so clocks and "
+                         "power settle")
+    ap.add_argument("--config", type=int, default=3, choices=[1, 2, 3, 4, 5])
+    ap.add_argument("--also", default="auto",
+                    help="further workloads measured in the same run, reported under per_config: a comma list, "
+                         "'none', or 'auto' (the other workloads of 2-5)")
     ap.add_argument("--layers", type=int, default=0, help="KV copies cycled by the steps (0: enough to exceed 1 GiB)")
     ap.add_argument("--path", type=int, default=0, help="0 auto, 1 vector, 2 matrix cores")
     ap.add_argument("--splits", type=int, default=0, help="forced KV ranges per request (queue/grid schedules)")
@@ -88,9 +101,8 @@ def kernel_source_hash() -> str:
 def measured_traffic(cfg: int):
     """(HBM bytes, algorithmic bytes) of one decode launch from the committed
     rocprofv3 counter summary of this workload (scaled FETCH_SIZE +
-    WRITE_SIZE, and the algorithmic bytes of the counted launches, whose
-    contexts are close to but not exactly those of this run), or (None,
-    None) when there is none or the kernel sources changed since."""
+    WRITE_SIZE, and the algorithmic bytes of the counted launches), or
+    (None, None) when there is none or the kernel sources changed since."""
     path = os.path.join(ROOT, "profiles", PROFILE_NAMES.get(cfg, "") + ".json")
     if not os.path.exists(path):
         return None, None
@@ -165,47 +177,50 @@ def cpu_baseline(wl, budget_s: float):
     }
 
 
-def main():
-    args = parse()
-    if args.gpus != 1:
-        print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported (the path does not shard).",
-              file=sys.stderr)
-        sys.exit(2)
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def measure(cfg: int, args) -> dict:
+    """Loads workload cfg, settles the clocks, runs the warmup steps, then
+    the timed throughput pass and the kernel-timing pass; returns the
+    record of this workload."""
     import torch
 
-    from paper_2606_24506_amd import crosspool as cpl
     from workloads import make_workload
     from workloads.harness import load, to_device_u16
 
-    assert torch.cuda.is_available(), "bench.py needs a GPU"
-    wl = make_workload(args.config)
+    wl = make_workload(cfg)
+    B = len(wl.requests)
     kv_bytes = sum(rq.ctx_len * wl.model(r).kappa for r, rq in enumerate(wl.requests))
     layers = args.layers or max(1, math.ceil((1 << 30) / kv_bytes))
-    max_warmup = args.warmup if args.warmup >= 0 else MAX_AUTO_WARMUP
-    total_steps = max_warmup + 2 * args.steps  # warmup, throughput pass, kernel-timing pass
-    grow = -(-total_steps // layers) + 1
-    print(f"[bench] cfg{args.config}: {len(wl.requests)} requests, {kv_bytes / 1e6:.1f} MB KV per layer, "
-          f"{layers} layers", file=sys.stderr, flush=True)
+    n_warm = args.warmup
+    # appends each layer sees before its first timed step
+    pre = [len(range(li, n_warm, layers)) for li in range(layers)]
+    grow = -(-(n_warm + 2 * args.steps) // layers) + 2
+    log(f"cfg{cfg}: {B} requests, {kv_bytes / 1e6:.1f} MB KV per layer, {layers} layers")
 
-    rows_cache = {r: wl.rows_bits(r) for r in range(len(wl.requests))}
-    inter = 512 if args.config == 4 else (4096 if args.config == 5 else 0)
+    rows_full = {r: wl.rows_bits(r) for r in range(B)}
+    inter = 512 if cfg == 4 else (4096 if cfg == 5 else 0)
     if args.planes:
         if wl.filler_pages:
             sys.exit("--planes: the filler requests of this pool leave no room for more than one KV plane")
         # one pool, L planes: step i serves layer i % L of every request
-        one = load(wl, reserve_extra=grow, interleave=inter, rows_override=rows_cache,
+        short = n_warm // layers + 1
+        one = load(wl, reserve_extra=grow, interleave=inter,
+                   rows_override={r: x[:max(1, x.shape[0] - short)] for r, x in rows_full.items()},
                    placement_seed=wl.placement_seed, backing=args.backing, n_layers=layers)
         lds = [one] * layers
     else:
-        lds = [load(wl, reserve_extra=grow, interleave=inter, rows_override=rows_cache,
-                    placement_seed=wl.placement_seed + 1000 * i, backing=args.backing) for i in range(layers)]
-    del rows_cache
-    B = len(wl.requests)
+        lds = []
+        for li in range(layers):
+            # one token short of the configured context after this layer's warmup appends
+            rows_li = {r: x[:max(1, x.shape[0] - pre[li] - 1)] for r, x in rows_full.items()}
+            lds.append(load(wl, reserve_extra=grow, interleave=inter, rows_override=rows_li,
+                            placement_seed=wl.placement_seed + 1000 * li, backing=args.backing))
+    del rows_full
     # one new token per request per step: seeded rows, resident on the GPU before timing
-    new_rows = []
-    for r in range(B):
-        new_rows.append(wl.step_rows_bits(r, 0).reshape(-1))
-    new_rows = to_device_u16(np.concatenate(new_rows), "cuda")
+    new_rows = to_device_u16(np.concatenate([wl.step_rows_bits(r, 0).reshape(-1) for r in range(B)]), "cuda")
     ones = [1] * B
     stream = torch.cuda.current_stream()
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
@@ -213,39 +228,43 @@ def main():
         a.record(stream)
         b.record(stream)
     torch.cuda.synchronize()
+    opts = dict(num_splits=args.splits, path=args.path, schedule=args.schedule)
 
     def step(i, evs=None):
         ld = lds[i % layers]
-        opts = dict(num_splits=args.splits, path=args.path, schedule=args.schedule)
+        o = dict(opts)
         if evs is not None:
-            opts.update(ev_begin=evs[0].cuda_event, ev_end=evs[1].cuda_event)
+            o.update(ev_begin=evs[0].cuda_event, ev_end=evs[1].cuda_event)
         if args.unfused:
             ld.pool.append(ld.req_ids, ones, new_rows, stream)
-            ld.pool.decode(ld.req_ids, ld.q, ld.out, ld.lse, stream, **opts)
+            ld.pool.decode(ld.req_ids, ld.q, ld.out, ld.lse, stream, **o)
         else:
-            ld.pool.decode_step(ld.req_ids, ones, new_rows, ld.q, ld.out, ld.lse, stream, **opts)
+            ld.pool.decode_step(ld.req_ids, ones, new_rows, ld.q, ld.out, ld.lse, stream, **o)
 
     if args.copy_mib:
         src = torch.empty(args.copy_mib << 20, dtype=torch.uint8, device="cuda")
         dst = torch.empty_like(src)
         dst.copy_(src)
         del src, dst
-    # Warmup. The attention kernels of the 128-head batches draw enough power
-    # that the clocks take tens of milliseconds of continuous work to settle
-    # after an idle gap, so by default the warmup lasts a fixed GPU time: 20
-    # steps measure the step time, then one unbroken run fills the rest.
-    n_warm = args.warmup if args.warmup >= 0 else min(20, MAX_AUTO_WARMUP)
-    t0 = time.perf_counter()
+    # Clock settling: the attention kernels of the 128-head batches draw
+    # enough power that the clocks take tens of milliseconds of continuous
+    # work to settle after an idle gap. Decode-only calls (no appends, so no
+    # context grows) fill args.settle_seconds of GPU time.
+    settle = 0
+    if args.settle_seconds > 0:
+        t0 = time.perf_counter()
+        for i in range(10):
+            ld = lds[i % layers]
+            ld.pool.decode(ld.req_ids, ld.q, ld.out, ld.lse, stream, **opts)
+        torch.cuda.synchronize()
+        per = (time.perf_counter() - t0) / 10
+        settle = 10 + max(0, min(MAX_SETTLE_CALLS, math.ceil(args.settle_seconds / per)) - 10)
+        for i in range(10, settle):
+            ld = lds[i % layers]
+            ld.pool.decode(ld.req_ids, ld.q, ld.out, ld.lse, stream, **opts)
     for i in range(n_warm):
         step(i)
     torch.cuda.synchronize()
-    if args.warmup < 0 and n_warm > 0:
-        per_step = (time.perf_counter() - t0) / n_warm
-        more = min(MAX_AUTO_WARMUP, math.ceil(args.warmup_seconds / per_step)) - n_warm
-        for i in range(n_warm, n_warm + max(0, more)):
-            step(i)
-        n_warm += max(0, more)
-        torch.cuda.synchronize()
     ctx0 = [[ld.pool.ctx_len(r) for r in ld.req_ids] for ld in lds]
     if args.planes:  # tokens in flight through the planes count for the layers they reached
         ctx0 = [[c + (li < lds[0].pool.cursor(r)[0]) for c, r in zip(ctx0[li], lds[0].req_ids)]
@@ -270,10 +289,13 @@ def main():
     pct = lambda q: kern_each[min(len(kern_each) - 1, int(q * len(kern_each)))]
     # algorithmic bytes of the two timed passes (contexts grow by one per visit)
     dec_bytes, app_bytes, dec_bytes_timed, dec_flops_timed = 0, 0, 0, 0
+    first_ctx = None
     visits = [0] * layers
     for i in range(2 * args.steps):
         li = (n_warm + i) % layers
         ctx = [c + visits[li] + 1 for c in ctx0[li]]
+        if first_ctx is None:
+            first_ctx = ctx
         visits[li] += 1
         if i < args.steps:
             dec_bytes += algorithmic_bytes_decode(wl, ctx)
@@ -281,29 +303,23 @@ def main():
         else:
             dec_bytes_timed += algorithmic_bytes_decode(wl, ctx)
             dec_flops_timed += algorithmic_flops_decode(wl, ctx)
+    configured = [rq.ctx_len for rq in wl.requests]
 
     value = (dec_bytes + app_bytes) / wall / 1e9
     ms_per_step = wall * 1e3 / args.steps
     achieved = dec_bytes_timed / args.steps / (kern_ms * 1e-3) / 1e9
     tflops = dec_flops_timed / args.steps / (kern_ms * 1e-3) / 1e12
-    traffic, traffic_alg = measured_traffic(args.config)
-    res = {
-        "metric": "paged decode-attention achieved HBM GB/s and req-tokens/s on 1 MI355X",
+    traffic, traffic_alg = measured_traffic(cfg)
+    rec = {
         "value": round(value, 2),
-        "unit": "GB/s",
-        "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": n_warm,
         "ms_per_step": round(ms_per_step, 5),
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": "bf16",
-        "data": "synthetic (seeded draws shaped like the workload; no dataset)",
         "config": {
-            "workload": WORKLOAD_NAMES[args.config],
+            "workload": WORKLOAD_NAMES[cfg],
             "requests": B,
-            "context_tokens": int(sum(ctx0[0])),
+            "context_tokens_configured": int(sum(configured)),
+            "context_tokens_first_timed_step": int(sum(first_ctx)),
+            "first_timed_step_at_configured_lengths": (not args.planes) and list(first_ctx) == configured,
+            "context_growth_per_timed_pass": -(-args.steps // layers),
             "kv_bytes_per_step": int(kv_bytes),
             "layers_cycled": layers,
             "step": ("cp_kv_append (1 token/request) + cp_attn_decode" if args.unfused
@@ -312,13 +328,14 @@ def main():
             "schedule": ["balanced", "queue", "grid"][args.schedule],
             "backing": ["buffer", "virtual"][args.backing],
             "layers_as": "KV planes of one pool (layer cursor)" if args.planes else "one pool per layer",
+            "settle_calls": settle,
         },
         "req_tokens_per_s": round(B / (wall / args.steps), 1),
         "host_enqueue_ms_per_step": round(t_enq * 1e3 / args.steps, 5),
         "context_tokens_per_s": round(sum(ctx0[0]) / (wall / args.steps), 1),
         "roofline": {
             "bound": "hbm",
-            "kernel": "decode attention (cp_attn_decode main launch, merge excluded)",
+            "kernel": KERNEL_NAMES.get(cfg, "decode attention") + ": cp_attn_decode's attention launch, merge excluded",
             "achieved": round(achieved, 2),
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
@@ -330,6 +347,14 @@ def main():
             "kernel_ms": round(kern_ms, 5),
             "kernel_ms_p10_p50_p90": [round(pct(0.1), 5), round(pct(0.5), 5), round(pct(0.9), 5)],
         },
+        # the whole step (fused append, attention, split merge, launch gaps)
+        # against the same roofline: decode bytes per step over the
+        # throughput pass's wall time per step
+        "whole_step": {
+            "achieved": round(dec_bytes / args.steps / (ms_per_step * 1e-3) / 1e9, 2),
+            "unit": "GB/s",
+            "frac": round(dec_bytes / args.steps / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+        },
         # the same kernel's attention arithmetic against the dense bf16
         # matrix-core peak (the many-head MLA batches are the ones near it)
         "matrix": {
@@ -339,10 +364,67 @@ def main():
             "frac": round(tflops / MFMA_BF16_PEAK_TFLOPS, 4),
         },
     }
-    if not args.no_cpu_baseline:
-        res["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
+    log(f"cfg{cfg}: kernel {kern_ms * 1e3:.1f} us, {achieved:.0f} GB/s ({achieved / HBM_PEAK_GBS:.3f}), "
+        f"step {ms_per_step * 1e3:.1f} us")
     for ld in (lds[:1] if args.planes else lds):
         ld.close()
+    del lds
+    torch.cuda.empty_cache()
+    return rec
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported (the path does not shard).",
+              file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    from paper_2606_24506_amd import crosspool as cpl  # noqa: F401  (fails loudly without the built library)
+    from workloads import make_workload
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    if args.also == "auto":
+        also = [c for c in (2, 3, 4, 5) if c != args.config] if args.config in (2, 3, 4, 5) else []
+    elif args.also in ("", "none"):
+        also = []
+    else:
+        also = [int(x) for x in args.also.split(",") if x and int(x) != args.config]
+
+    head = measure(args.config, args)
+    per_config = {}
+    for c in also:
+        r = measure(c, args)
+        per_config[str(c)] = {"workload": WORKLOAD_NAMES[c], "value": r["value"], "unit": "GB/s",
+                              "ms_per_step": r["ms_per_step"], "req_tokens_per_s": r["req_tokens_per_s"],
+                              "host_enqueue_ms_per_step": r["host_enqueue_ms_per_step"],
+                              "roofline": r["roofline"], "whole_step": r["whole_step"], "matrix": r["matrix"],
+                              "config": r["config"]}
+    res = {
+        "metric": "paged decode-attention achieved HBM GB/s and req-tokens/s on 1 MI355X",
+        "value": head["value"],
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": head["ms_per_step"],
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded draws shaped like the workload; no dataset)",
+        "config": head["config"],
+        "req_tokens_per_s": head["req_tokens_per_s"],
+        "host_enqueue_ms_per_step": head["host_enqueue_ms_per_step"],
+        "context_tokens_per_s": head["context_tokens_per_s"],
+        "roofline": head["roofline"],
+        "whole_step": head["whole_step"],
+        "matrix": head["matrix"],
+        "per_config": per_config,
+    }
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline(make_workload(args.config), args.cpu_seconds)
     print(json.dumps(res))
 
 

@@ -121,6 +121,12 @@ typedef struct {
   /* Maximum number of simultaneously open requests; 0 means 4096. */
   int32_t max_requests;
   int32_t backing; /* cp_backing */
+  /* Cap on the device memory the pool may hold for split-KV partial
+   * results (the per-range outputs and lse values a long request's decode
+   * merges); 0 means no cap. A decode whose split plan needs more fails
+   * with CP_ENOMEM before anything is enqueued or any state changes; the
+   * queue and grid schedules with num_splits = 1 need none. */
+  uint64_t max_workspace_bytes;
 } cp_pool_desc;
 
 /* Create a pool. Errors: CP_EINVAL (page_tokens not in [1, 4096],

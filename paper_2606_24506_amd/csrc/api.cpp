@@ -76,8 +76,7 @@ struct AppendPlan {
   uint32_t pte = 0;   // entry of the new page
 };
 cp_status decode_impl(cp_pool *p, int32_t n, const int32_t *req_ids, const void *q, void *out, float *lse,
-                      void *hip_stream, const cp_decode_opts *opts, const void *rows,
-                      const std::vector<AppendPlan> *app);
+                      void *hip_stream, const cp_decode_opts *opts);
 }  // namespace
 
 struct cp_pool {
@@ -98,6 +97,7 @@ struct cp_pool {
   uint16_t *ws_o = nullptr;  // split partial outputs (bf16)
   float *ws_l = nullptr;
   uint64_t ws_o_cap = 0, ws_l_cap = 0;  // elements
+  uint64_t ws_limit = 0;                // bytes of workspace the pool may hold (0: no cap)
   std::vector<void *> ws_retired;         // outgrown workspaces, freed with the pool
   int num_cus = 256;
 };
@@ -235,6 +235,7 @@ cp_status cp_pool_create(const cp_pool_desc *d, cp_pool **out) {
   }
   p->device = d->device;
   p->host_only = d->device < 0;
+  p->ws_limit = d->max_workspace_bytes;
   if (!p->host_only) {
     int ndev = 0;
     if (hipGetDeviceCount(&ndev) != hipSuccess || d->device >= ndev) {
@@ -653,14 +654,27 @@ int32_t units_per_range(const Geom &g, const GeomK &k) {
 // lse values.
 cp_status ensure_ws(cp_pool *p, uint64_t o_elems, uint64_t l_floats) {
   if (o_elems <= p->ws_o_cap && l_floats <= p->ws_l_cap) return CP_OK;
+  const uint64_t need_bytes = o_elems * sizeof(uint16_t) + l_floats * sizeof(float);
+  if (p->ws_limit && need_bytes > p->ws_limit)
+    return fail(CP_ENOMEM, "the split plan needs %llu bytes of workspace, past the pool's cap of %llu",
+                (unsigned long long)need_bytes, (unsigned long long)p->ws_limit);
   // Growth allocates twice what is asked, so that the slow drift of split
   // plans as contexts grow rarely repeats it, and keeps the old buffers
   // until the pool is destroyed: kernels already queued may still use them,
   // and freeing them here would stall the host until the device drains.
+  // With a cap, growth takes what is asked and no more, and outgrown
+  // buffers are not kept: the cap bounds the bytes held.
   auto grow = [&](auto **buf, uint64_t *cap, uint64_t need) -> cp_status {
     if (need <= *cap) return CP_OK;
-    const uint64_t c = std::max<uint64_t>(2 * need, 2 * *cap);
+    const uint64_t c = p->ws_limit ? need : std::max<uint64_t>(2 * need, 2 * *cap);
     void *nb = nullptr;
+    if (p->ws_limit && *buf) {
+      // queued kernels may still read the old buffer: drain the device first
+      (void)hipDeviceSynchronize();
+      (void)hipFree(*buf);
+      *buf = nullptr;
+      *cap = 0;
+    }
     if (hipMalloc(&nb, c * sizeof(**buf)) != hipSuccess) return fail(CP_ENOMEM, "workspace allocation failed");
     if (*buf) p->ws_retired.push_back(*buf);
     *buf = static_cast<std::remove_reference_t<decltype(*buf)>>(nb);
@@ -678,7 +692,7 @@ extern "C" {
 
 cp_status cp_attn_decode_ex(cp_pool *p, int32_t n, const int32_t *req_ids, const void *q, void *out, float *lse,
                             void *hip_stream, const cp_decode_opts *opts) {
-  return decode_impl(p, n, req_ids, q, out, lse, hip_stream, opts, nullptr, nullptr);
+  return decode_impl(p, n, req_ids, q, out, lse, hip_stream, opts);
 }
 
 }  // extern "C"
@@ -732,38 +746,62 @@ cp_status decode_prepare(cp_pool *p, int32_t n, const int32_t *req_ids, const vo
   return CP_OK;
 }
 
-// The decode of cp_attn_decode_ex; with `app` (one entry per request, call
-// order) the launches also perform the fused appends of cp_attn_decode_step.
-cp_status decode_impl(cp_pool *p, int32_t n, const int32_t *req_ids, const void *q, void *out, float *lse,
-                      void *hip_stream, const cp_decode_opts *opts, const void *rows,
-                      const std::vector<AppendPlan> *app) {
+// Everything one decode call launches: per-request offsets, launch groups,
+// split plan and workspace layout. Built and checked in full before any
+// pool state changes or anything is enqueued.
+struct DecodePlan {
+  struct Group {
+    std::vector<int32_t> idx;
+    std::vector<int32_t> models;  // pool model ids, launch-local order
+    uint32_t mask = 0;
+    int grid = 0;
+    uint32_t total_cost = 0;
+    uint32_t n_units = 0;
+  };
   cp_decode_opts o{};
   std::vector<GeomK> gk;
-  cp_status rc = decode_prepare(p, n, req_ids, q, out, lse, opts, &o, &gk);
-  if (rc) return rc;
+  std::vector<int64_t> attend;  // tokens each request attends over (call order)
+  std::vector<uint64_t> q_off, o_off, l_off;
+  std::vector<Group> groups;
+  std::vector<int32_t> n_slots, chunk_pages, first_worker, hblk;
+  std::vector<uint32_t> cost_prefix, ws_base, ws_orow;
+  uint64_t ws_rows = 0, ws_elems = 0;  // partial lse rows and partial output elements
+  uint16_t *ws_o = nullptr;            // bound by the caller before launch
+  float *ws_l = nullptr;
+};
+
+// Plans a decode over requests whose attended lengths are their current
+// ones plus extra[i] (tokens a fused step places before the launch; NULL:
+// none). pl->o and pl->gk come from decode_prepare. Runs every capacity
+// check of the call; changes nothing.
+cp_status plan_decode(cp_pool *p, int32_t n, const int32_t *req_ids, const int32_t *extra, DecodePlan *pl) {
+  const cp_decode_opts &o = pl->o;
+  const std::vector<GeomK> &gk = pl->gk;
   const int32_t P = p->st.page_tokens();
+  auto model_of = [&](int32_t i) { return p->st.req(req_ids[i]).model; };
+  pl->attend.assign(n, 0);
   for (int32_t i = 0; i < n; ++i) {
-    const Request &r = p->st.req(req_ids[i]);
-    if (r.attend_len() < 1) return fail(CP_EINVAL, "request %d has an empty context", req_ids[i]);
+    pl->attend[i] = p->st.req(req_ids[i]).attend_len() + (extra ? extra[i] : 0);
+    if (pl->attend[i] < 1) return fail(CP_EINVAL, "request %d has an empty context", req_ids[i]);
   }
 
   // Packed offsets in call order.
-  std::vector<uint64_t> q_off(n), o_off(n), l_off(n);
+  pl->q_off.assign(n, 0);
+  pl->o_off.assign(n, 0);
+  pl->l_off.assign(n, 0);
   std::vector<int64_t> pages(n);
   uint64_t qo = 0, oo = 0, lo = 0;
   for (int32_t i = 0; i < n; ++i) {
-    const Request &r = p->st.req(req_ids[i]);
-    const Geom &g = p->st.model(r.model);
-    q_off[i] = qo;
-    o_off[i] = oo;
-    l_off[i] = lo;
+    const Geom &g = p->st.model(model_of(i));
+    pl->q_off[i] = qo;
+    pl->o_off[i] = oo;
+    pl->l_off[i] = lo;
     qo += (uint64_t)g.hq * g.d_k;
     oo += (uint64_t)g.hq * g.d_v;
     lo += (uint64_t)g.hq;
-    pages[i] = (r.attend_len() + P - 1) / P;
+    pages[i] = (pl->attend[i] + P - 1) / P;
   }
   if (qo > 0xFFFFFFFFull || oo > 0xFFFFFFFFull) return fail(CP_EINVAL, "batch too large");
-  auto model_of = [&](int32_t i) { return p->st.req(req_ids[i]).model; };
   // kernel family: vector variants share a launch, narrow matrix variants
   // share another, and each wide variant has a kernel of its own
   auto wclass = [&](int32_t i) {
@@ -778,15 +816,9 @@ cp_status decode_impl(cp_pool *p, int32_t n, const int32_t *req_ids, const void 
   std::vector<int32_t> order(n);
   for (int32_t i = 0; i < n; ++i) order[i] = i;
   std::stable_sort(order.begin(), order.end(), [&](int32_t x, int32_t y) { return wclass(x) < wclass(y); });
-  struct Group {
-    std::vector<int32_t> idx;
-    std::vector<int32_t> models;  // pool model ids, launch-local order
-    uint32_t mask = 0;
-    int grid = 0;
-    uint32_t total_cost = 0;
-    uint32_t n_units = 0;
-  };
-  std::vector<Group> groups;
+  using Group = DecodePlan::Group;
+  std::vector<Group> &groups = pl->groups;
+  groups.clear();
   for (int32_t k = 0; k < n;) {
     Group g;
     const int cls = wclass(order[k]);
@@ -803,12 +835,15 @@ cp_status decode_impl(cp_pool *p, int32_t n, const int32_t *req_ids, const void 
   }
 
   // Per-request plan: partial slots and the fields the kernels read.
-  std::vector<int32_t> n_slots(n, 1), chunk_pages(n, 0), first_worker(n, 0), hblk(n, 1);
-  std::vector<uint32_t> cost_prefix(n, 0);
-  for (int32_t i = 0; i < n; ++i) {
-    const Geom &g = p->st.model(model_of(i));
-    hblk[i] = units_per_range(g, gk[model_of(i)]);
-  }
+  std::vector<int32_t> &n_slots = pl->n_slots, &chunk_pages = pl->chunk_pages, &first_worker = pl->first_worker,
+                       &hblk = pl->hblk;
+  std::vector<uint32_t> &cost_prefix = pl->cost_prefix;
+  n_slots.assign(n, 1);
+  chunk_pages.assign(n, 0);
+  first_worker.assign(n, 0);
+  hblk.assign(n, 1);
+  cost_prefix.assign(n, 0);
+  for (int32_t i = 0; i < n; ++i) hblk[i] = units_per_range(p->st.model(model_of(i)), gk[model_of(i)]);
   for (Group &g : groups) {
     const bool wide = g.mask && is_wide_variant(__builtin_ctz(g.mask));
     const int wgs = wide ? 1 : decode_wgs_per_cu(g.mask);
@@ -835,6 +870,7 @@ cp_status decode_impl(cp_pool *p, int32_t n, const int32_t *req_ids, const void 
       }
       g.grid = (int)W;
       g.total_cost = (uint32_t)T;
+      if (g.grid > 0xFFFF) return fail(CP_EINVAL, "too many workers");
     } else {
       // queue / grid: page-aligned KV ranges of similar cost, about two per
       // workgroup slot (one when every request is a 128-head matrix model,
@@ -847,7 +883,7 @@ cp_status decode_impl(cp_pool *p, int32_t n, const int32_t *req_ids, const void 
         const int32_t v = gk[model_of(i)].variant;
         all_wide = all_wide && is_wide_variant(v);
         any_matrix = any_matrix || v >= kMatrixFirst;
-        pin.push_back(PlanIn{model_of(i), p->st.req(req_ids[i]).attend_len()});
+        pin.push_back(PlanIn{model_of(i), pl->attend[i]});
         hb.push_back(hblk[i]);
       }
       std::vector<Geom> geoms;
@@ -880,29 +916,49 @@ cp_status decode_impl(cp_pool *p, int32_t n, const int32_t *req_ids, const void 
 
   // Workspace for requests split over several slots.
   uint64_t ws_rows = 0, ws_elems = 0;
-  std::vector<uint32_t> ws_base(n, kNoWs), ws_orow(n, 0);
+  pl->ws_base.assign(n, kNoWs);
+  pl->ws_orow.assign(n, 0);
   for (int32_t i = 0; i < n; ++i) {
     if (n_slots[i] <= 1) continue;
     const Geom &g = p->st.model(model_of(i));
-    ws_base[i] = (uint32_t)ws_rows;
+    pl->ws_base[i] = (uint32_t)ws_rows;
     ws_rows += (uint64_t)n_slots[i] * g.hq;
     ws_elems = (ws_elems + 511) / 512 * 512;
-    ws_orow[i] = (uint32_t)(ws_elems / (uint64_t)g.d_v);
+    pl->ws_orow[i] = (uint32_t)(ws_elems / (uint64_t)g.d_v);
     ws_elems += (uint64_t)n_slots[i] * g.hq * g.d_v;
   }
   if (ws_rows >= kNoWs || ws_elems / 64 >= kNoWs) return fail(CP_EINVAL, "split workspace too large");
+  pl->ws_rows = ws_rows;
+  pl->ws_elems = ws_elems;
+  return CP_OK;
+}
 
-  DeviceGuard dg(p->device);
-  hipStream_t s = (hipStream_t)hip_stream;
-  if (ws_rows) {
-    rc = ensure_ws(p, ws_elems, ws_rows);
+// Binds the pool's own split workspace to a plan, growing it if needed.
+cp_status bind_pool_workspace(cp_pool *p, DecodePlan *pl) {
+  if (pl->ws_rows) {
+    DeviceGuard dg(p->device);
+    cp_status rc = ensure_ws(p, pl->ws_elems, pl->ws_rows);
     if (rc) return rc;
   }
+  pl->ws_o = p->ws_o;
+  pl->ws_l = p->ws_l;
+  return CP_OK;
+}
+
+// Enqueues a planned decode: the attention launches (with `app`, one entry
+// per request in call order, they also perform the fused appends of
+// cp_attn_decode_step) and the merges of split requests. Only HIP failures
+// remain possible here.
+cp_status launch_plan(cp_pool *p, const DecodePlan &pl, int32_t n, const int32_t *req_ids, const void *q,
+                      void *out, float *lse, void *hip_stream, const void *rows, const std::vector<AppendPlan> *app) {
+  const cp_decode_opts &o = pl.o;
+  DeviceGuard dg(p->device);
+  hipStream_t s = (hipStream_t)hip_stream;
   // The caller's events take the start of the first decode launch and the
   // end of the last one (timestamps of the launches themselves, no marker
   // packets between them).
-  for (size_t gi = 0; gi < groups.size(); ++gi) {
-    const Group &g = groups[gi];
+  for (size_t gi = 0; gi < pl.groups.size(); ++gi) {
+    const DecodePlan::Group &g = pl.groups[gi];
     DecodeArgs a{};
     a.pool = p->dev_pool;
     a.pte = p->dev_pte;
@@ -910,38 +966,37 @@ cp_status decode_impl(cp_pool *p, int32_t n, const int32_t *req_ids, const void 
     a.out = (uint16_t *)out;
     a.lse = lse;
     a.rows = (const uint16_t *)rows;
-    a.ws_o = p->ws_o;
-    a.ws_l = p->ws_l;
+    a.ws_o = pl.ws_o;
+    a.ws_l = pl.ws_l;
     a.queue = p->queue;
     a.schedule = o.schedule;
     a.total_cost = g.total_cost;
     a.n_units = (int32_t)g.n_units;
-    for (size_t k = 0; k < g.models.size(); ++k) a.geom[k] = gk[g.models[k]];
+    for (size_t k = 0; k < g.models.size(); ++k) a.geom[k] = pl.gk[g.models[k]];
     for (int32_t i : g.idx) {
       const Request &r = p->st.req(req_ids[i]);
       DecReq &d = a.req[a.n_req++];
       d.pte_base = r.plane_base(r.cursor);  // the KV plane of the request's current layer
-      d.ctx_len = (uint32_t)r.attend_len();
-      d.q_off = (uint32_t)q_off[i];
-      d.o_off = (uint32_t)o_off[i];
-      d.lse_off = (uint32_t)l_off[i];
-      d.ws_base = ws_base[i];
-      d.ws_orow = ws_orow[i];
-      d.unit_begin = cost_prefix[i];
-      d.chunk_pages = (uint16_t)(o.schedule == CP_SCHED_BALANCED ? first_worker[i] : chunk_pages[i]);
-      d.n_chunks = (uint16_t)n_slots[i];
+      d.ctx_len = (uint32_t)pl.attend[i];
+      d.q_off = (uint32_t)pl.q_off[i];
+      d.o_off = (uint32_t)pl.o_off[i];
+      d.lse_off = (uint32_t)pl.l_off[i];
+      d.ws_base = pl.ws_base[i];
+      d.ws_orow = pl.ws_orow[i];
+      d.unit_begin = pl.cost_prefix[i];
+      d.chunk_pages = (uint16_t)(o.schedule == CP_SCHED_BALANCED ? pl.first_worker[i] : pl.chunk_pages[i]);
+      d.n_chunks = (uint16_t)pl.n_slots[i];
       d.model = (uint8_t)(std::find(g.models.begin(), g.models.end(), r.model) - g.models.begin());
-      d.n_hblk = (uint16_t)hblk[i];
+      d.n_hblk = (uint16_t)pl.hblk[i];
       if (app) {
         d.app_flags = (*app)[i].flags;
         d.app_off = (*app)[i].off;
         d.app_pte = (*app)[i].pte;
       }
     }
-    if (g.grid > 0xFFFF && o.schedule == CP_SCHED_BALANCED) return fail(CP_EINVAL, "too many workers");
     const int v0 = __builtin_ctz(g.mask);
     const hipEvent_t ev0 = gi == 0 ? (hipEvent_t)o.ev_begin : nullptr;
-    const hipEvent_t ev1 = gi + 1 == groups.size() ? (hipEvent_t)o.ev_end : nullptr;
+    const hipEvent_t ev1 = gi + 1 == pl.groups.size() ? (hipEvent_t)o.ev_end : nullptr;
     hipError_t e = is_wide_variant(v0) ? launch_decode_wide(a, g.grid, v0, s, ev0, ev1)
                                        : launch_decode(a, g.grid, g.mask, s, ev0, ev1);
     if (e != hipSuccess) return hip_fail(e, "decode launch");
@@ -949,8 +1004,8 @@ cp_status decode_impl(cp_pool *p, int32_t n, const int32_t *req_ids, const void 
 
   // Merge launches for split requests.
   MergeArgs ma{};
-  ma.ws_o = p->ws_o;
-  ma.ws_l = p->ws_l;
+  ma.ws_o = pl.ws_o;
+  ma.ws_l = pl.ws_l;
   ma.out = (uint16_t *)out;
   ma.lse = lse;
   auto flush = [&]() -> cp_status {
@@ -962,25 +1017,38 @@ cp_status decode_impl(cp_pool *p, int32_t n, const int32_t *req_ids, const void 
     return CP_OK;
   };
   for (int32_t i = 0; i < n; ++i) {
-    if (ws_base[i] == kNoWs) continue;
+    if (pl.ws_base[i] == kNoWs) continue;
     if (ma.n_req == kMaxReqPerLaunch) {
-      rc = flush();
+      cp_status rc = flush();
       if (rc) return rc;
     }
-    const Geom &g = p->st.model(model_of(i));
+    const Geom &g = p->st.model(p->st.req(req_ids[i]).model);
     MergeReq &m = ma.req[ma.n_req++];
     m.block_begin = (uint32_t)ma.n_blocks;  // first merge workgroup of this request
     m.hq = (uint32_t)g.hq;
     m.d_v = (uint32_t)g.d_v;
-    m.n_chunks = (uint32_t)n_slots[i];
-    m.ws_base = ws_base[i];
-    m.ws_orow = ws_orow[i];
-    m.o_off = (uint32_t)o_off[i];
-    m.lse_off = (uint32_t)l_off[i];
+    m.n_chunks = (uint32_t)pl.n_slots[i];
+    m.ws_base = pl.ws_base[i];
+    m.ws_orow = pl.ws_orow[i];
+    m.o_off = (uint32_t)pl.o_off[i];
+    m.lse_off = (uint32_t)pl.l_off[i];
     // one workgroup per (head, block of V columns)
     ma.n_blocks += g.hq * (int32_t)((uint32_t)g.d_v / merge_block_cols((uint32_t)g.d_v));
   }
   return flush();
+}
+
+// The decode of cp_attn_decode_ex.
+cp_status decode_impl(cp_pool *p, int32_t n, const int32_t *req_ids, const void *q, void *out, float *lse,
+                      void *hip_stream, const cp_decode_opts *opts) {
+  DecodePlan pl;
+  cp_status rc = decode_prepare(p, n, req_ids, q, out, lse, opts, &pl.o, &pl.gk);
+  if (rc) return rc;
+  rc = plan_decode(p, n, req_ids, nullptr, &pl);
+  if (rc) return rc;
+  rc = bind_pool_workspace(p, &pl);
+  if (rc) return rc;
+  return launch_plan(p, pl, n, req_ids, q, out, lse, hip_stream, nullptr, nullptr);
 }
 
 }  // namespace
@@ -994,9 +1062,8 @@ cp_status cp_attn_decode(cp_pool *p, int32_t n, const int32_t *req_ids, const vo
 
 cp_status cp_attn_decode_step(cp_pool *p, int32_t n, const int32_t *req_ids, const int32_t *n_new, const void *rows,
                               const void *q, void *out, float *lse, void *hip_stream, const cp_decode_opts *opts) {
-  cp_decode_opts o{};
-  std::vector<GeomK> gk;
-  cp_status rc = decode_prepare(p, n, req_ids, q, out, lse, opts, &o, &gk);
+  DecodePlan pl;
+  cp_status rc = decode_prepare(p, n, req_ids, q, out, lse, opts, &pl.o, &pl.gk);
   if (rc) return rc;
   if (!n_new) return fail(CP_EINVAL, "null n_new");
   bool any = false;
@@ -1020,14 +1087,6 @@ cp_status cp_attn_decode_step(cp_pool *p, int32_t n, const int32_t *req_ids, con
     any = any || n_new[i] != 0;
   }
   if (any && !rows) return fail(CP_EINVAL, "null rows");
-  auto advance_all = [&] {
-    for (int32_t i = 0; i < n; ++i) p->st.advance(req_ids[i]);
-  };
-  if (!any) {
-    rc = cp_attn_decode_ex(p, n, req_ids, q, out, lse, hip_stream, opts);
-    if (rc == CP_OK) advance_all();
-    return rc;
-  }
   uint64_t total_elems = 0;
   std::vector<int32_t> placing(n, 0);  // new tokens, placed at the first layer
   for (int32_t i = 0; i < n; ++i) {
@@ -1037,6 +1096,21 @@ cp_status cp_attn_decode_step(cp_pool *p, int32_t n, const int32_t *req_ids, con
     placing[i] = r.cursor == 0 ? 1 : 0;
   }
   if (total_elems > 0xFFFFFFFFull) return fail(CP_EINVAL, "too many rows in one call");
+  // The whole launch is planned, checked and its workspace bound at the
+  // lengths the step will attend over, before any page is allocated: a
+  // refused call changes nothing.
+  rc = plan_decode(p, n, req_ids, placing.data(), &pl);
+  if (rc) return rc;
+  rc = bind_pool_workspace(p, &pl);
+  if (rc) return rc;
+  auto advance_all = [&] {
+    for (int32_t i = 0; i < n; ++i) p->st.advance(req_ids[i]);
+  };
+  if (!any) {
+    rc = launch_plan(p, pl, n, req_ids, q, out, lse, hip_stream, nullptr, nullptr);
+    if (rc == CP_OK) advance_all();
+    return rc;
+  }
   rc = prepare_growth(p, n, req_ids, placing.data());
   if (rc) return rc;
 
@@ -1073,10 +1147,11 @@ cp_status cp_attn_decode_step(cp_pool *p, int32_t n, const int32_t *req_ids, con
     off += (uint64_t)p->st.model(r.model).row_elems;
   }
   rc = push_ptes(p, lo_rest, hi_rest, s);
-  if (rc == CP_OK) rc = decode_impl(p, n, req_ids, q, out, lse, hip_stream, &o, rows, &plan);
+  if (rc == CP_OK) rc = launch_plan(p, pl, n, req_ids, q, out, lse, hip_stream, rows, &plan);
   if (rc) {
-    // keep the device pool in step with the host tables: write the new page
-    // entries and rows the unfused way (rewriting a fused row is harmless)
+    // a HIP failure after the tokens were placed: keep the device pool in
+    // step with the host tables by writing the new page entries and rows
+    // the unfused way (rewriting a fused row is harmless)
     const std::string msg = cp_last_error();
     std::vector<AppItem> items;
     for (int32_t i = 0; i < n; ++i) {

@@ -91,3 +91,69 @@ def test_decode_step_without_appends_is_decode():
         assert a.pool.ctx_len(a.req_ids[0]) == 300  # rejected calls change nothing
     finally:
         a.close()
+
+
+def test_refused_step_changes_nothing():
+    """A step whose split plan needs more workspace than the pool may hold
+    (max_workspace_bytes) is refused with CP_ENOMEM before any page is
+    allocated: context lengths, cursors, page tables and pool statistics
+    stay as they were. The same step then runs unsplit (one KV range per
+    request needs no workspace) and appends exactly once."""
+    lens = [("mla16", 4096), ("mqa32", 1000)]  # 4096: the new token opens a page
+    wl = custom(lens, seed=13)
+    pool = cpl.Pool(page_tokens=64, pool_bytes=wl.pool_bytes, chunk_bytes=wl.chunk_bytes, placement_seed=3,
+                    device=0, max_workspace_bytes=4096)
+    mids = {m: pool.register_spec(MODELS[m]) for m in wl.models_used()}
+    rids = [pool.open(mids[rq.model], rq.ctx_len + 8) for rq in wl.requests]
+    rows = [wl.rows_bits(r) for r in range(len(lens))]
+    for rid, rw in zip(rids, rows):
+        pool.append([rid], [rw.shape[0]], to_device_u16(rw, "cuda"))
+    q = to_device_u16(np.concatenate([x.reshape(-1) for x in wl.q_bits]), "cuda")
+    out = torch.zeros(sum(MODELS[m].n_q_heads * MODELS[m].d_v for m, _ in lens), dtype=torch.int16, device="cuda")
+    lse = torch.zeros(sum(MODELS[m].n_q_heads for m, _ in lens), dtype=torch.float32, device="cuda")
+    rng = np.random.default_rng(14)
+    new = [normal_bf16(rng, (1, wl.model(r).row_width), 0.7) for r in range(len(lens))]
+    new_dev = to_device_u16(np.concatenate([x.reshape(-1) for x in new]), "cuda")
+
+    def state():
+        return ([pool.ctx_len(r) for r in rids], [pool.cursor(r) for r in rids],
+                [pool.pages(r).tolist() for r in rids], pool.stats())
+
+    try:
+        torch.cuda.synchronize()
+        before = state()
+        for fn in (lambda: pool.decode_step(rids, [1, 1], new_dev, q, out, lse),  # balanced: splits
+                   lambda: pool.decode_step(rids, [1, 1], new_dev, q, out, lse, schedule=cpl.CP_SCHED_QUEUE,
+                                            num_splits=3),
+                   lambda: pool.decode(rids, q, out, lse, schedule=cpl.CP_SCHED_GRID)):
+            with pytest.raises(cpl.CrossPoolError) as e:
+                fn()
+            assert e.value.status == cpl.CP_ENOMEM
+            assert state() == before
+        pool.decode_step(rids, [1, 1], new_dev, q, out, lse, schedule=cpl.CP_SCHED_QUEUE, num_splits=1)
+        torch.cuda.synchronize()
+        assert [pool.ctx_len(r) for r in rids] == [n + 1 for _, n in lens]
+        for r, rid in enumerate(rids):
+            full = np.concatenate([rows[r], new[r]])
+            dst = torch.empty(full.size, dtype=torch.int16, device="cuda")
+            pool.gather(rid, 0, full.shape[0], dst)
+            torch.cuda.synchronize()
+            assert np.array_equal(_bits(dst).reshape(full.shape), full)
+
+        class _View:
+            def out_bits(self, r):
+                off = sum(MODELS[m].n_q_heads * MODELS[m].d_v for m, _ in lens[:r])
+                m = wl.model(r)
+                return _bits(out)[off:off + m.n_q_heads * m.d_v].reshape(m.n_q_heads, m.d_v)
+
+            def lse_of(self, r):
+                off = sum(MODELS[m].n_q_heads for m, _ in lens[:r])
+                return lse.cpu().numpy()[off:off + wl.model(r).n_q_heads].astype(np.float64)
+
+        compare(_View(), {r: expected_for(wl, r, rows=np.concatenate([rows[r], new[r]])) for r in range(len(lens))},
+                "refused then unsplit step")
+    finally:
+        torch.cuda.synchronize()
+        for r in rids:
+            pool.close(r)
+        pool.destroy()
