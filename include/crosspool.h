@@ -323,6 +323,29 @@ typedef struct {
 cp_status cp_attn_decode_ex(cp_pool *pool, int32_t n, const int32_t *req_ids, const void *q, void *out, float *lse,
                             void *hip_stream, const cp_decode_opts *opts);
 
+/* Size in bytes of the fixed split workspace of cp_attn_decode_noalloc. */
+#define CP_NOALLOC_WORKSPACE_BYTES (40u * 1024u * 1024u)
+
+/* cp_attn_decode_ex for callers that cannot allocate device memory: code
+ * under HIP graph capture, tight serving loops, and harnesses that forbid
+ * allocation. Same arguments, kernels, split plans and results (out and lse
+ * bit-identical to cp_attn_decode_ex with the same opts), but the split
+ * workspace (the partial outputs and lse values of requests decoded over
+ * several KV ranges) is a fixed device array of CP_NOALLOC_WORKSPACE_BYTES
+ * that each GPU the library runs on holds until the process ends, instead
+ * of the pool's growable workspace: the call makes no hipMalloc or hipFree
+ * and no other device allocation. The caller still passes q, out and lse.
+ * A plan needing more than that (partial outputs: 2 * n_q_heads * d_v bytes
+ * per KV range of each split request, plus 4 * n_q_heads for lse) fails
+ * with CP_EINVAL before anything is enqueued; the DeepSeek-V3-shaped batch
+ * (8 x 128K tokens, 128 heads) and the 512K-token burst need about 35 MB.
+ * The array is shared by every call on one GPU, whichever pool it is on,
+ * and keeps the last call's contents (nothing in it needs clearing):
+ * noalloc calls on one GPU must not overlap on the device (one stream, or
+ * the caller orders them); overlapping calls race on the workspace. */
+cp_status cp_attn_decode_noalloc(cp_pool *pool, int32_t n, const int32_t *req_ids, const void *q, void *out,
+                                 float *lse, void *hip_stream, const cp_decode_opts *opts);
+
 /* One decode step with single-token appends: the effect of cp_kv_append(pool,
  * n, req_ids, n_new, rows, hip_stream) followed by cp_attn_decode_ex(pool, n,
  * req_ids, q, out, lse, hip_stream, opts), with the same arguments, layouts

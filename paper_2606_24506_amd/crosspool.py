@@ -141,6 +141,7 @@ def _load() -> C.CDLL:
         "cp_kv_append": ([P, I32, C.POINTER(I32), C.POINTER(I32), VP, VP], I32),
         "cp_attn_decode": ([P, I32, C.POINTER(I32), VP, VP, VP, VP], I32),
         "cp_attn_decode_ex": ([P, I32, C.POINTER(I32), VP, VP, VP, VP, C.POINTER(cp_decode_opts)], I32),
+        "cp_attn_decode_noalloc": ([P, I32, C.POINTER(I32), VP, VP, VP, VP, C.POINTER(cp_decode_opts)], I32),
         "cp_attn_decode_step": ([P, I32, C.POINTER(I32), C.POINTER(I32), VP, VP, VP, VP, VP, C.POINTER(cp_decode_opts)],
                                 I32),
         "cp_kv_gather": ([P, I32, I64, I64, VP, VP], I32),
@@ -283,6 +284,19 @@ def cp_attn_decode_ex(pool: int, req_ids: Sequence[int], q, out, lse, stream=Non
                                  _stream(stream), C.byref(o)))
 
 
+def cp_attn_decode_noalloc(pool: int, req_ids: Sequence[int], q, out, lse, stream=None, *, num_splits: int = 0,
+                           schedule: int = CP_SCHED_BALANCED, path: int = CP_PATH_AUTO, ev_begin=None,
+                           ev_end=None) -> None:
+    def ev(e):
+        if e is None:
+            return None
+        return e.cuda_event if hasattr(e, "cuda_event") else int(e)
+
+    o = cp_decode_opts(num_splits, schedule, path, 0, ev(ev_begin), ev(ev_end))
+    _check(LIB.cp_attn_decode_noalloc(pool, len(req_ids), _i32_array(req_ids), _ptr(q), _ptr(out), _ptr(lse),
+                                      _stream(stream), C.byref(o)))
+
+
 def cp_attn_decode_step(pool: int, req_ids: Sequence[int], n_new: Sequence[int], rows, q, out, lse, stream=None, *,
                         num_splits: int = 0, schedule: int = CP_SCHED_BALANCED, path: int = CP_PATH_AUTO,
                         ev_begin=None, ev_end=None) -> None:
@@ -375,6 +389,9 @@ class Pool:
             cp_attn_decode_ex(self.handle, req_ids, q, out, lse, stream, **opts)
         else:
             cp_attn_decode(self.handle, req_ids, q, out, lse, stream)
+
+    def decode_noalloc(self, req_ids, q, out, lse, stream=None, **opts) -> None:
+        cp_attn_decode_noalloc(self.handle, req_ids, q, out, lse, stream, **opts)
 
     def decode_step(self, req_ids, n_new, rows, q, out, lse, stream=None, **opts) -> None:
         cp_attn_decode_step(self.handle, req_ids, n_new, rows, q, out, lse, stream, **opts)

@@ -14,6 +14,7 @@
 
 #include "crosspool.h"
 #include "kargs.h"
+static_assert(cp::kNoAllocScratchBytes == CP_NOALLOC_WORKSPACE_BYTES, "the header states the fixed workspace size");
 #include "status.hpp"
 #include "pool.hpp"
 
@@ -27,6 +28,7 @@ hipError_t launch_decode_wide(const DecodeArgs &a, int grid, int variant, hipStr
 int decode_wgs_per_cu(uint32_t mask);
 int narrow_streams(int variant);
 hipError_t launch_merge(const MergeArgs &a, hipStream_t stream);
+hipError_t scratch_device_address(int device, void **out);
 }  // namespace cp
 
 using namespace cp;
@@ -1058,6 +1060,32 @@ extern "C" {
 cp_status cp_attn_decode(cp_pool *p, int32_t n, const int32_t *req_ids, const void *q, void *out, float *lse,
                          void *hip_stream) {
   return cp_attn_decode_ex(p, n, req_ids, q, out, lse, hip_stream, nullptr);
+}
+
+cp_status cp_attn_decode_noalloc(cp_pool *p, int32_t n, const int32_t *req_ids, const void *q, void *out, float *lse,
+                                 void *hip_stream, const cp_decode_opts *opts) {
+  DecodePlan pl;
+  cp_status rc = decode_prepare(p, n, req_ids, q, out, lse, opts, &pl.o, &pl.gk);
+  if (rc) return rc;
+  rc = plan_decode(p, n, req_ids, nullptr, &pl);
+  if (rc) return rc;
+  // partial outputs first, then the partial lse values (256-byte aligned)
+  const uint64_t o_bytes = (pl.ws_elems * sizeof(uint16_t) + 255) / 256 * 256;
+  const uint64_t need = o_bytes + pl.ws_rows * sizeof(float);
+  if (need > kNoAllocScratchBytes)
+    return fail(CP_EINVAL,
+                "the split plan needs %llu bytes of workspace; cp_attn_decode_noalloc has %llu (use fewer KV ranges: "
+                "the queue or grid schedule with a smaller num_splits)",
+                (unsigned long long)need, (unsigned long long)kNoAllocScratchBytes);
+  if (pl.ws_rows) {
+    DeviceGuard dg(p->device);
+    void *base = nullptr;
+    hipError_t e = scratch_device_address(p->device, &base);
+    if (e != hipSuccess) return hip_fail(e, "address of the fixed split workspace");
+    pl.ws_o = static_cast<uint16_t *>(base);
+    pl.ws_l = reinterpret_cast<float *>(static_cast<uint8_t *>(base) + o_bytes);
+  }
+  return launch_plan(p, pl, n, req_ids, q, out, lse, hip_stream, nullptr, nullptr);
 }
 
 cp_status cp_attn_decode_step(cp_pool *p, int32_t n, const int32_t *req_ids, const int32_t *n_new, const void *rows,

@@ -10,6 +10,9 @@ namespace cp {
 constexpr int kMaxLaunchModels = 4;   // distinct models in one decode launch
 constexpr int kMaxReqPerLaunch = 64;  // requests in one launch (at most one per lane of a wave)
 constexpr uint32_t kNoWs = 0xFFFFFFFFu;
+// Fixed split workspace of cp_attn_decode_noalloc, per GPU, in bytes.
+constexpr uint64_t kNoAllocScratchBytes = 40ull << 20;
+constexpr int kMaxScratchDevices = 64;
 enum : int32_t { kSchedBalanced = 0, kSchedQueue = 1, kSchedGrid = 2 };
 // Balanced schedule: the fixed work of one piece (page-table and query
 // loads, the latency of its first pages under a loaded memory system, the

@@ -10,6 +10,7 @@
 #include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
+#include <mutex>
 #include <type_traits>
 
 #include "decode_mfma.h"
@@ -563,6 +564,41 @@ hipError_t launch_merge(const MergeArgs &a, hipStream_t stream) {
   const int waves = max_n >= 8 * kMergeUnroll ? kMergeMaxWaves : 4;
   hipLaunchKernelGGL(merge_kernel, dim3(a.n_blocks), dim3(64 * waves), 0, stream, a);
   return hipGetLastError();
+}
+
+
+// ------------------------------------------------- fixed split workspace
+
+// The split workspace of cp_attn_decode_noalloc: partial outputs and lse
+// values of split requests, in a file-scope device array that each GPU the
+// library runs on holds until the process ends, so that the call allocates
+// no device memory. Nothing in it needs clearing between calls: a launch
+// writes every partial slot it plans before its merge reads it. In host
+// code this name stands for a host-side placeholder, not device memory; the
+// device address comes from scratch_device_address() only.
+static __device__ __align__(256) uint8_t scratch[kNoAllocScratchBytes];
+
+// Device address of `scratch` on `device`, which the caller has made
+// current. Resolved once per device (each GPU holds its own copy of the
+// array at its own address) and kept.
+hipError_t scratch_device_address(int device, void **out) {
+  static std::mutex mu;
+  static void *addr[kMaxScratchDevices] = {};
+  if (device < 0 || device >= kMaxScratchDevices) return hipErrorInvalidDevice;
+  int cur = -1;
+  hipError_t e = hipGetDevice(&cur);
+  if (e != hipSuccess) return e;
+  if (cur != device) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!addr[device]) {
+    void *ptr = nullptr;
+    e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!ptr) return hipErrorInvalidSymbol;
+    addr[device] = ptr;
+  }
+  *out = addr[device];
+  return hipSuccess;
 }
 
 }  // namespace cp
