@@ -64,6 +64,8 @@ def parse():
                     help="further workloads measured in the same run, reported under per_config: a comma list, "
                          "'none', or 'auto' (the other workloads of 2-5)")
     ap.add_argument("--layers", type=int, default=0, help="KV copies cycled by the steps (0: enough to exceed 1 GiB)")
+    ap.add_argument("--ctx-scale", type=float, default=1.0,
+                    help="scale every context length of the workload (1: the configured sizes)")
     ap.add_argument("--path", type=int, default=0, help="0 auto, 1 vector, 2 matrix cores")
     ap.add_argument("--splits", type=int, default=0, help="forced KV ranges per request (queue/grid schedules)")
     ap.add_argument("--schedule", type=int, default=0, help="0 balanced, 1 work queue, 2 one workgroup per unit")
@@ -190,7 +192,9 @@ def measure(cfg: int, args) -> dict:
     from workloads import make_workload
     from workloads.harness import load, to_device_u16
 
-    wl = make_workload(cfg)
+    wl = make_workload(cfg, scale_ctx=args.ctx_scale)
+    if args.ctx_scale != 1.0 and wl.filler_pages:
+        wl.filler_pages = int(wl.filler_pages * args.ctx_scale)
     B = len(wl.requests)
     kv_bytes = sum(rq.ctx_len * wl.model(r).kappa for r, rq in enumerate(wl.requests))
     layers = args.layers or max(1, math.ceil((1 << 30) / kv_bytes))

@@ -851,12 +851,28 @@ cp_status plan_decode(cp_pool *p, int32_t n, const int32_t *req_ids, const int32
     const int wgs = wide ? 1 : decode_wgs_per_cu(g.mask);
     const int64_t slots = (int64_t)p->num_cus * wgs;
     if (o.schedule == CP_SCHED_BALANCED) {
-      uint64_t T = 0, maxc = 1;
+      // Every workgroup pays the fixed cost of its first piece, so the cost
+      // line charges kPieceFixedCost only where a request boundary falls
+      // inside a workgroup's share (that workgroup runs a second piece):
+      // not before the launch's first request, and not at a boundary that
+      // coincides with a share boundary of the line without fixed costs
+      // (equal requests over a multiple of their count of workgroups).
+      uint64_t T0 = 0, maxc = 1;
       for (int32_t i : g.idx) {
         const uint64_t c = (uint64_t)gk[model_of(i)].page_cost;
-        cost_prefix[i] = (uint32_t)T;
-        T += kPieceFixedCost + (uint64_t)pages[i] * c;
+        T0 += (uint64_t)pages[i] * c;
         maxc = std::max(maxc, c);
+      }
+      const uint64_t W0 = std::max<uint64_t>(1, std::min<uint64_t>((uint64_t)slots, T0 / maxc));
+      uint64_t T = 0, pre0 = 0;
+      for (size_t k = 0; k < g.idx.size(); ++k) {
+        const int32_t i = g.idx[k];
+        const uint64_t c = (uint64_t)gk[model_of(i)].page_cost;
+        const bool straddled = k > 0 && (pre0 * W0) % T0 != 0;
+        T += straddled ? kPieceFixedCost : 0;
+        cost_prefix[i] = (uint32_t)std::min<uint64_t>(T, 0xFFFFFFFFull);  // the request's first page
+        T += (uint64_t)pages[i] * c;
+        pre0 += (uint64_t)pages[i] * c;
       }
       if (T > 0xFFFFFFFFull) return fail(CP_EINVAL, "batch too large for one launch");
       // every range spans at least one page of any model, so no request has
@@ -864,8 +880,8 @@ cp_status plan_decode(cp_pool *p, int32_t n, const int32_t *req_ids, const int32
       const uint64_t W = std::max<uint64_t>(1, std::min<uint64_t>((uint64_t)slots, T / maxc));
       auto owner = [&](uint64_t x) { return (uint32_t)(((x + 1) * W - 1) / T); };
       for (int32_t i : g.idx) {
-        // page j of the request sits at C + j c, after the fixed cost
-        const uint64_t c = (uint64_t)gk[model_of(i)].page_cost, C = cost_prefix[i] + kPieceFixedCost;
+        // page j of the request sits at C + j c
+        const uint64_t c = (uint64_t)gk[model_of(i)].page_cost, C = cost_prefix[i];
         const uint32_t w0 = owner(C), w1 = owner(C + (uint64_t)(pages[i] - 1) * c);
         first_worker[i] = (int32_t)w0;
         n_slots[i] = (int32_t)(w1 - w0 + 1);

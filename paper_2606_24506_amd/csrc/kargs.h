@@ -18,9 +18,11 @@ enum : int32_t { kSchedBalanced = 0, kSchedQueue = 1, kSchedGrid = 2 };
 // loads, the latency of its first pages under a loaded memory system, the
 // end merge and the partial write), in page-cost units (8 KiB of page
 // bytes each): measured at about 23K cycles per piece on the narrow kernel,
-// which streams about 600 cycles per unit. Each request's stretch of the
-// cost line starts with that much cost, so a workgroup whose share crosses
-// into another request takes correspondingly fewer pages.
+// which streams about 600 cycles per unit. A request boundary that falls
+// inside a workgroup's share is preceded by that much cost on the cost
+// line, so the workgroup that runs a second piece there takes
+// correspondingly fewer pages. DecReq::unit_begin is the cost position of
+// the request's first page.
 constexpr uint32_t kPieceFixedCost = 40;
 
 // Decode code paths (GeomK::variant), chosen per model by the host.
@@ -67,7 +69,7 @@ struct DecReq {
   uint32_t lse_off;   // float offset of its log-sum-exp values
   uint32_t ws_base;   // first partial lse row (kNoWs when the request is not split)
   uint32_t ws_orow;   // partial outputs start at element offset ws_orow * d_v
-  uint32_t unit_begin;   // queue/grid: first unit; balanced: cost prefix of the request
+  uint32_t unit_begin;   // queue/grid: first unit; balanced: cost position of the request's first page
   uint16_t chunk_pages;  // queue/grid: pages per KV range; balanced: first worker of the request
   uint16_t n_chunks;     // KV ranges = partial slots
   uint8_t model;         // index into DecodeArgs::geom

@@ -21,8 +21,9 @@ __device__ __forceinline__ bool next_balanced(const DecodeArgs &a, int *r, uint3
   for (; *r < a.n_req; ++*r, *hb = 0) {
     const DecReq &rq = a.req[*r];
     const GeomK &gm = a.geom[rq.model];
-    // the request's pages start after its fixed cost
-    const uint64_t c = (uint64_t)gm.page_cost, C = rq.unit_begin + kPieceFixedCost;
+    // the request's pages start at its cost prefix (any fixed cost of a
+    // piece that starts there comes before it)
+    const uint64_t c = (uint64_t)gm.page_cost, C = rq.unit_begin;
     if (C >= L1) return false;
     const uint64_t pages = (rq.ctx_len + gm.page_tokens - 1) / gm.page_tokens;
     if (C + pages * c <= L0) continue;
