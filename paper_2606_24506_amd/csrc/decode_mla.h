@@ -37,10 +37,10 @@
 //
 // Registers are the binding limit (the P.V accumulators and the query
 // fragments take 200 of a wave's 256), so per-lane constants are formed
-// where they are used, from an opaque copy of the lane index taken each
-// iteration: the compiler can neither hoist them out of the loop nor keep
-// them in scratch memory, whose reloads would make it wait for every load
-// in flight, tile loads included.
+// where they are used, from the lane index counted afresh each iteration:
+// the compiler can neither hoist them out of the loop nor keep them in
+// scratch memory, whose reloads would make it wait for every load in
+// flight, tile loads included.
 #pragma once
 
 #include "decode_mfma.h"
@@ -76,16 +76,16 @@ struct MlaCfg {
 CP_DEV int mla_vswz(int r) { return (2 * r) & 15; }
 CP_DEV int mla_rswz(int r) { return r & 6; }
 
-// Lane index and its mfma coordinates, from a copy the compiler cannot see
-// through.
+// Lane index and its mfma coordinates, counted afresh by the lane-count
+// instructions at every use: the compiler can neither hoist them nor keep
+// the thread index alive across the loop for them.
 struct LaneIds {
   int lane, col, quad;
 };
-CP_DEV LaneIds lane_ids(int tid) {
+CP_DEV LaneIds lane_ids() {
   int t;
-  asm volatile("v_mov_b32 %0, %1" : "=v"(t) : "v"(tid));
-  const int lane = t & 63;
-  return LaneIds{lane, lane & 15, lane >> 4};
+  asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(t));
+  return LaneIds{t, t & 15, t >> 4};
 }
 
 __device__ __forceinline__ void mla_unit(const DecodeArgs &a, const GeomK &gm, const DecReq &rq, const Seg &sg,
@@ -95,7 +95,7 @@ __device__ __forceinline__ void mla_unit(const DecodeArgs &a, const GeomK &gm, c
   const uint32_t slot = sg.slot;
   const int tid = threadIdx.x;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const LaneIds L0 = lane_ids(tid);
+  const LaneIds L0 = lane_ids();
   const int lane = L0.lane, col = L0.col, quad = L0.quad;
   const int P = gm.page_tokens;  // the host routes only pages of a multiple of 32 tokens here
   const int tpp = P / T;
@@ -116,7 +116,7 @@ __device__ __forceinline__ void mla_unit(const DecodeArgs &a, const GeomK &gm, c
   uint32_t pte_lane = 0;
   int pte_batch = -1;
   auto load_ptes = [&](int batch) {
-    const int sp = batch * 64 + lane;
+    const int sp = batch * 64 + lane_ids().lane;
     pte_lane = sp < npg ? a.pte[rq.pte_base + pg_begin + (uint32_t)sp] : 0u;
     pte_batch = batch;
     // a visible wait: the tile loads are inline asm the compiler cannot
@@ -271,7 +271,7 @@ __device__ __forceinline__ void mla_unit(const DecodeArgs &a, const GeomK &gm, c
     // tile k visible; P^T and rescale record of tile k-1 complete; the value
     // slot of tile k-2 and the rotary slot of tile k-1 are free
     __syncthreads();
-    const LaneIds L = lane_ids(tid);
+    const LaneIds L = lane_ids();
     const int lane = L.lane, col = L.col, quad = L.quad;
     const int kn = k + 2;
     const bool more = loader && kn < ntiles;
@@ -289,7 +289,7 @@ __device__ __forceinline__ void mla_unit(const DecodeArgs &a, const GeomK &gm, c
         const int nz = (T - valid) * (C::MROW / 16);
         uint32_t z;  // a zero formed here, not a zero vector kept through the loop
         asm volatile("v_mov_b32 %0, 0" : "=v"(z));
-        for (int i = tid; i < nz; i += 64 * NW)
+        for (int i = wave * 64 + lane; i < nz; i += 64 * NW)
           *reinterpret_cast<uint4 *>(vt + valid * C::MROW + i * 16) = make_uint4(z, z, z, z);
       }
 
@@ -373,6 +373,9 @@ __device__ __forceinline__ void mla_unit(const DecodeArgs &a, const GeomK &gm, c
   }
 
   // ---- final: score waves publish m and l; every wave normalises its columns
+  {
+  const LaneIds Lf = lane_ids();
+  const int lane = Lf.lane, col = Lf.col, quad = Lf.quad;
   lsum = xor_sum_16_32(lsum);
   __syncthreads();  // every wave is past its last P.V: the rescale records are free
   float *const m_x = reinterpret_cast<float *>(xbuf + C::XFLAGS);
@@ -403,6 +406,7 @@ __device__ __forceinline__ void mla_unit(const DecodeArgs &a, const GeomK &gm, c
       a.ws_l[(uint64_t)rq.ws_base + (uint64_t)slot * gm.hq + head] = lse;
     else
       a.lse[rq.lse_off + head] = lse;
+  }
   }
   __syncthreads();  // LDS is reused by the next unit
 }
