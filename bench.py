@@ -76,6 +76,8 @@ def parse():
     ap.add_argument("--planes", action="store_true",
                     help="one pool whose models have one KV plane per layer, the steps moving each request's "
                          "layer cursor, instead of one pool per layer")
+    ap.add_argument("--device-pages", action="store_true",
+                    help="pools with device free-page stacks: the steps pop new pages inside the launch")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="target CPU time of the oracle sample")
     ap.add_argument("--copy-mib", type=int, default=0,
@@ -213,7 +215,8 @@ def measure(cfg: int, args) -> dict:
         short = n_warm // layers + 1
         one = load(wl, reserve_extra=grow, interleave=inter,
                    rows_override={r: x[:max(1, x.shape[0] - short)] for r, x in rows_full.items()},
-                   placement_seed=wl.placement_seed, backing=args.backing, n_layers=layers)
+                   placement_seed=wl.placement_seed, backing=args.backing, n_layers=layers,
+                   device_pages=int(args.device_pages))
         lds = [one] * layers
     else:
         lds = []
@@ -221,7 +224,8 @@ def measure(cfg: int, args) -> dict:
             # one token short of the configured context after this layer's warmup appends
             rows_li = {r: x[:max(1, x.shape[0] - pre[li] - 1)] for r, x in rows_full.items()}
             lds.append(load(wl, reserve_extra=grow, interleave=inter, rows_override=rows_li,
-                            placement_seed=wl.placement_seed + 1000 * li, backing=args.backing))
+                            placement_seed=wl.placement_seed + 1000 * li, backing=args.backing,
+                            device_pages=int(args.device_pages)))
     del rows_full
     # one new token per request per step: seeded rows, resident on the GPU before timing
     new_rows = to_device_u16(np.concatenate([wl.step_rows_bits(r, 0).reshape(-1) for r in range(B)]), "cuda")
@@ -331,6 +335,7 @@ def measure(cfg: int, args) -> dict:
             "path": ["auto", "vector", "matrix"][args.path],
             "schedule": ["balanced", "queue", "grid"][args.schedule],
             "backing": ["buffer", "virtual"][args.backing],
+            "new_pages": "device free-page stacks" if args.device_pages else "host allocation",
             "layers_as": "KV planes of one pool (layer cursor)" if args.planes else "one pool per layer",
             "settle_calls": settle,
         },

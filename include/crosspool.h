@@ -127,6 +127,20 @@ typedef struct {
    * with CP_ENOMEM before anything is enqueued or any state changes; the
    * queue and grid schedules with num_splits = 1 need none. */
   uint64_t max_workspace_bytes;
+  /* 0: cp_attn_decode_step allocates a new token's pages on the host and
+   * passes their page-table entries in the launch. 1: each model has a
+   * free-page stack in device memory, and the step's launch pops a new
+   * token's pages (one per KV plane) from it and writes their entries into
+   * the device page table itself (Section 3.3, control lowering; the
+   * per-token path then does no host page bookkeeping). The host refills a
+   * stack, with up to a chunk's worth of pages, before a step that would
+   * empty it; pages in a stack count against their model's reservations.
+   * The host copy of the popped entries is read back, waiting for the
+   * device, at the next cp_request_pages, cp_request_close or cp_kv_append;
+   * a close also returns stack pages no open reservation can still use.
+   * Results do not depend on this setting. A step may open at most 7168
+   * pages of one model (requests times planes). */
+  int32_t device_pages;
 } cp_pool_desc;
 
 /* Create a pool. Errors: CP_EINVAL (page_tokens not in [1, 4096],

@@ -43,6 +43,7 @@ class cp_pool_desc(C.Structure):
         ("max_requests", C.c_int32),
         ("backing", C.c_int32),
         ("max_workspace_bytes", C.c_uint64),
+        ("device_pages", C.c_int32),
     ]
 
 
@@ -198,9 +199,9 @@ def cp_version() -> int:
 
 def cp_pool_create(page_tokens: int = 64, pool_bytes: int = 0, chunk_bytes: int = 0, placement_seed: int = 0,
                    device: int = 0, device_mem=None, max_requests: int = 0, backing: int = 0,
-                   max_workspace_bytes: int = 0) -> int:
+                   max_workspace_bytes: int = 0, device_pages: int = 0) -> int:
     d = cp_pool_desc(page_tokens, device, pool_bytes, chunk_bytes, placement_seed, _ptr(device_mem), max_requests,
-                     backing, max_workspace_bytes)
+                     backing, max_workspace_bytes, device_pages)
     out = C.c_void_p()
     _check(LIB.cp_pool_create(C.byref(d), C.byref(out)))
     return out.value

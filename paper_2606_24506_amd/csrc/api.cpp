@@ -28,6 +28,7 @@ hipError_t launch_decode_wide(const DecodeArgs &a, int grid, int variant, hipStr
 int decode_wgs_per_cu(uint32_t mask);
 int narrow_streams(int variant);
 hipError_t launch_merge(const MergeArgs &a, hipStream_t stream);
+hipError_t launch_stack_push(const StackPushArgs &a, hipStream_t stream);
 hipError_t scratch_device_address(int device, void **out);
 }  // namespace cp
 
@@ -73,9 +74,9 @@ struct DeviceGuard {
 
 // One fused append of cp_attn_decode_step, per request in call order.
 struct AppendPlan {
-  uint8_t flags = 0;  // kAppRow, kAppPage
+  uint8_t flags = 0;  // kAppRow, kAppPage, kAppPop
   uint32_t off = 0;   // element offset of the row in the caller's rows
-  uint32_t pte = 0;   // entry of the new page
+  uint32_t pte = 0;   // entry of the new page (kAppPop: the request id)
 };
 cp_status decode_impl(cp_pool *p, int32_t n, const int32_t *req_ids, const void *q, void *out, float *lse,
                       void *hip_stream, const cp_decode_opts *opts);
@@ -102,6 +103,20 @@ struct cp_pool {
   uint64_t ws_limit = 0;                // bytes of workspace the pool may hold (0: no cap)
   std::vector<void *> ws_retired;         // outgrown workspaces, freed with the pool
   int num_cus = 256;
+  // Device page stacks (desc.device_pages): per model kStackCap entries,
+  // their counts, per-request pop state and plane strides. The host keeps
+  // each stack's entries [0, depth) (bottom first: the device pops from the
+  // top, so these are the ones still there) and the page-table slots that
+  // steps filled on the device and that it has not read back yet.
+  bool dev_pages = false;
+  bool broken = false;  // a step's launch failed after its pops were booked
+  uint32_t *dev_stack = nullptr;
+  int32_t *dev_top = nullptr;
+  uint32_t *dev_pop = nullptr;
+  uint32_t *dev_plane = nullptr;
+  uint32_t epoch = 0;
+  std::vector<std::vector<uint32_t>> stk;
+  std::vector<uint64_t> pending;
 };
 
 namespace {
@@ -186,6 +201,99 @@ cp_status vmm_setup(cp_pool *p, int dev) {
   return CP_OK;
 }
 
+// ---------------------------------------------------- device page stacks
+// (Section 3.3, control lowering: the pool's per-token page allocation runs
+// on the device; Section 3.1 keeps the host's mapping work off the
+// per-token path.)
+
+// Reads the page-table entries that decode steps wrote on the device back
+// into the host mirror. Waits for the device; a slow-path call.
+cp_status reconcile_pages(cp_pool *p) {
+  if (p->pending.empty()) return CP_OK;
+  DeviceGuard g(p->device);
+  hipError_t e = hipDeviceSynchronize();
+  if (e != hipSuccess) return hip_fail(e, "waiting for the device before reading back popped page entries");
+  const uint64_t lo = *std::min_element(p->pending.begin(), p->pending.end());
+  const uint64_t hi = *std::max_element(p->pending.begin(), p->pending.end()) + 1;
+  std::vector<uint32_t> dev(hi - lo);
+  e = hipMemcpy(dev.data(), p->dev_pte + lo, (hi - lo) * 4, hipMemcpyDeviceToHost);
+  if (e != hipSuccess) return hip_fail(e, "reading back popped page entries");
+  uint32_t *mirror = p->st.pte_mirror_mut();
+  for (uint64_t slot : p->pending) mirror[slot] = dev[slot - lo];
+  p->pending.clear();
+  return CP_OK;
+}
+
+// Enqueues the refill of model m's device stack with `fresh` on top of its
+// `depth` remaining entries.
+cp_status push_stack(cp_pool *p, int32_t m, int64_t depth, const std::vector<uint32_t> &fresh, hipStream_t s) {
+  StackPushArgs a{};
+  a.top = p->dev_top + m;
+  int64_t done = 0;
+  do {
+    const int32_t k = (int32_t)std::min<int64_t>(kStackPushMax, (int64_t)fresh.size() - done);
+    a.dst = p->dev_stack + (uint64_t)m * kStackCap + (uint64_t)(depth + done);
+    a.n = k;
+    std::copy(fresh.begin() + done, fresh.begin() + done + k, a.ent);
+    done += k;
+    a.new_top = (int32_t)(depth + done);
+    hipError_t e = launch_stack_push(a, s);
+    if (e != hipSuccess) return hip_fail(e, "device page stack refill");
+  } while (done < (int64_t)fresh.size());
+  return CP_OK;
+}
+
+// Before a step that pops need[m] pages of model m: refills every stack
+// that holds fewer, with at least a chunk's worth of pages (capped by the
+// stack and by what the model's reservations may still take). Pages taken
+// for a stack count against the reservations like request pages, so they
+// cannot push the pool past its budget. On failure nothing is enqueued.
+cp_status refill_stacks(cp_pool *p, const std::vector<int64_t> &need, hipStream_t s) {
+  for (int32_t m = 0; m < p->st.n_models(); ++m) {
+    std::vector<uint32_t> &st = p->stk[(size_t)m];
+    const int64_t depth = (int64_t)st.size();
+    if (need[(size_t)m] <= depth) continue;
+    const Geom &g = p->st.model(m);
+    int64_t k = std::max<int64_t>(need[(size_t)m] - depth, std::min<int64_t>(g.ppc, kStackRefill));
+    k = std::min<int64_t>({k, p->st.stack_room(m), kStackCap - depth});
+    if (depth + k < need[(size_t)m])  // unreachable: every pop is within a reservation
+      return fail(CP_ESTATE, "device page stack of model %d cannot hold the pages this step needs", m);
+    std::vector<int32_t> carved;
+    if (!p->st.ensure_slots(m, k, &carved)) {
+      p->st.release_empty(carved);
+      return fail(CP_ENOMEM, "could not map physical memory for %lld pages of model %d", (long long)k, m);
+    }
+    std::vector<uint32_t> fresh;
+    p->st.take_pages(m, k, &fresh);
+    cp_status rc = push_stack(p, m, depth, fresh, s);
+    if (rc) {
+      p->st.return_pages(fresh);
+      return rc;
+    }
+    st.insert(st.end(), fresh.begin(), fresh.end());
+  }
+  return CP_OK;
+}
+
+// After request id of model m closes (or is about to): gives back the
+// stack's top entries beyond what the model's open reservations may still
+// take, so that pages in a stack never hold chunks the budget owes to
+// other models. Waits for the device.
+cp_status drain_stack(cp_pool *p, int32_t m, int64_t room) {
+  std::vector<uint32_t> &st = p->stk[(size_t)m];
+  if ((int64_t)st.size() <= room) return CP_OK;
+  DeviceGuard g(p->device);
+  hipError_t e = hipDeviceSynchronize();
+  if (e != hipSuccess) return hip_fail(e, "waiting for the device before draining a page stack");
+  const int32_t top = (int32_t)std::max<int64_t>(0, room);
+  e = hipMemcpy(p->dev_top + m, &top, 4, hipMemcpyHostToDevice);
+  if (e != hipSuccess) return hip_fail(e, "lowering a device page stack");
+  std::vector<uint32_t> back(st.begin() + top, st.end());
+  st.resize((size_t)top);
+  p->st.return_pages(back);
+  return CP_OK;
+}
+
 // Carves, before any page is allocated, the chunks that growing the
 // requests by n_new tokens needs, so that the allocation itself cannot
 // fail. (A virtual pool mapped these at admission; this then carves
@@ -238,6 +346,12 @@ cp_status cp_pool_create(const cp_pool_desc *d, cp_pool **out) {
   p->device = d->device;
   p->host_only = d->device < 0;
   p->ws_limit = d->max_workspace_bytes;
+  if (d->device_pages != 0 && d->device_pages != 1) {
+    delete p;
+    return fail(CP_EINVAL, "device_pages must be 0 or 1");
+  }
+  p->dev_pages = d->device_pages == 1;
+  p->stk.assign(16, {});
   if (!p->host_only) {
     int ndev = 0;
     if (hipGetDeviceCount(&ndev) != hipSuccess || d->device >= ndev) {
@@ -272,6 +386,16 @@ cp_status cp_pool_create(const cp_pool_desc *d, cp_pool **out) {
               hipHostMalloc((void **)&p->pin_pte, nptes * 4, hipHostMallocDefault) == hipSuccess &&
               hipMalloc((void **)&p->queue, 64 * sizeof(uint32_t)) == hipSuccess;
     if (ok) ok = hipMemset(p->dev_pte, 0, nptes * 4) == hipSuccess && hipMemset(p->queue, 0, 64 * 4) == hipSuccess;
+    if (ok && d->device_pages) {
+      const uint64_t nm = 16, nr = (uint64_t)p->st.max_requests();
+      ok = hipMalloc((void **)&p->dev_stack, nm * kStackCap * 4) == hipSuccess &&
+           hipMalloc((void **)&p->dev_top, nm * 4) == hipSuccess &&
+           hipMalloc((void **)&p->dev_pop, nr * 4) == hipSuccess &&
+           hipMalloc((void **)&p->dev_plane, nr * 4) == hipSuccess;
+      if (ok)
+        ok = hipMemset(p->dev_top, 0, nm * 4) == hipSuccess && hipMemset(p->dev_pop, 0, nr * 4) == hipSuccess &&
+             hipMemset(p->dev_plane, 0, nr * 4) == hipSuccess;
+    }
     if (ok) std::memset(p->pin_pte, 0, nptes * 4);
     int cus = 0;
     if (ok && hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, d->device) == hipSuccess && cus > 0)
@@ -303,6 +427,8 @@ cp_status cp_pool_destroy(cp_pool *p) {
     if (p->dev_pte) (void)hipFree(p->dev_pte);
     if (p->pin_pte) (void)hipHostFree(p->pin_pte);
     if (p->queue) (void)hipFree(p->queue);
+    for (void *b : {(void *)p->dev_stack, (void *)p->dev_top, (void *)p->dev_pop, (void *)p->dev_plane})
+      if (b) (void)hipFree(b);
     if (p->ws_o) (void)hipFree(p->ws_o);
     if (p->ws_l) (void)hipFree(p->ws_l);
     for (void *w : p->ws_retired) (void)hipFree(w);
@@ -363,12 +489,32 @@ cp_status cp_request_open(cp_pool *p, int32_t model_id, int64_t reserve_tokens, 
   if (rc == -3) return fail(CP_ENOSPC, "%s", err.c_str());
   if (rc == -2) return fail(CP_ENOMEM, "%s", err.c_str());
   if (rc != 0) return fail(CP_EINVAL, "%s", err.c_str());
+  if (p->dev_pages && !p->host_only) {
+    // the plane stride the device pops use for this request id
+    DeviceGuard g(p->device);
+    const uint32_t plane = (uint32_t)p->st.req(*req_id).plane;
+    hipError_t e = hipMemcpy(p->dev_plane + *req_id, &plane, 4, hipMemcpyHostToDevice);
+    if (e != hipSuccess) {
+      p->st.close(*req_id);
+      return hip_fail(e, "recording the request's plane stride");
+    }
+  }
   return CP_OK;
 }
 
 cp_status cp_request_close(cp_pool *p, int32_t req_id) {
   if (!p) return fail(CP_EINVAL, "null pool");
   if (!p->st.valid_open(req_id)) return fail(CP_EINVAL, "request %d is not open", req_id);
+  cp_status rc = reconcile_pages(p);
+  if (rc) return rc;
+  if (p->dev_pages) {
+    // what the model's other open reservations may still take
+    const Request &r = p->st.req(req_id);
+    const int32_t m = r.model;
+    const int64_t room = p->st.stack_room(m) + p->st.in_stack(m) - (r.reserve_pages - r.pages_used * r.layers);
+    rc = drain_stack(p, m, room);
+    if (rc) return rc;
+  }
   p->vmm_synced = false;
   p->vmm_err = hipSuccess;
   p->st.close(req_id);
@@ -394,6 +540,8 @@ cp_status cp_request_cursor(cp_pool *p, int32_t req_id, int32_t *layer, int32_t 
 cp_status cp_request_pages(cp_pool *p, int32_t req_id, int64_t first, int64_t count, uint32_t *ptes) {
   if (!p || (!ptes && count > 0)) return fail(CP_EINVAL, "null argument");
   if (!p->st.valid_open(req_id)) return fail(CP_EINVAL, "request %d is not open", req_id);
+  cp_status rc = reconcile_pages(p);
+  if (rc) return rc;
   const Request &r = p->st.req(req_id);
   if (first < 0 || count < 0 || first + count > r.pages_used)
     return fail(CP_EINVAL, "page range [%lld, %lld) outside the %lld used pages", (long long)first,
@@ -423,6 +571,7 @@ GeomK geom_k(const Geom &g, int32_t P) {
   k.scale_log2 = g.scale * 1.4426950408889634f;
   k.variant = 0;
   k.nb = 1;
+  k.layers = g.layers;
   return k;
 }
 
@@ -508,6 +657,10 @@ cp_status cp_kv_append(cp_pool *p, int32_t n, const int32_t *req_ids, const int3
   cp_status rc = check_ids(p, n, req_ids);
   if (rc) return rc;
   if (n > 0 && !n_new) return fail(CP_EINVAL, "null n_new");
+  if (p->broken) return fail(CP_ESTATE, "a failed decode step left the device page stacks out of step; destroy the pool");
+  // the page-table copies below must not overwrite entries a step popped
+  rc = reconcile_pages(p);
+  if (rc) return rc;
   int64_t total = 0;
   for (int32_t i = 0; i < n; ++i) {
     if (n_new[i] < 0) return fail(CP_EINVAL, "negative n_new for request %d", req_ids[i]);
@@ -707,6 +860,7 @@ cp_status decode_prepare(cp_pool *p, int32_t n, const int32_t *req_ids, const vo
                          const cp_decode_opts *opts, cp_decode_opts *o_out, std::vector<GeomK> *gk_out) {
   if (!p) return fail(CP_EINVAL, "null pool");
   if (p->host_only) return fail(CP_ESTATE, "host-only pool cannot decode");
+  if (p->broken) return fail(CP_ESTATE, "a failed decode step left the device page stacks out of step; destroy the pool");
   if (n < 1) return fail(CP_EINVAL, "decode needs at least one request");
   cp_status rc = check_ids(p, n, req_ids);
   if (rc) return rc;
@@ -726,6 +880,7 @@ cp_status decode_prepare(cp_pool *p, int32_t n, const int32_t *req_ids, const vo
   for (int32_t m = 0; m < p->st.n_models(); ++m) {
     const Geom &g = p->st.model(m);
     gk[m] = geom_k(g, P);
+    gk[m].pool_model = m;
     const int32_t mv = o.path == CP_PATH_VALU ? -1 : matrix_variant(g, P);
     if (mv >= 0) {
       gk[m].variant = mv;
@@ -987,6 +1142,11 @@ cp_status launch_plan(cp_pool *p, const DecodePlan &pl, int32_t n, const int32_t
     a.ws_o = pl.ws_o;
     a.ws_l = pl.ws_l;
     a.queue = p->queue;
+    a.stack = p->dev_stack;
+    a.stack_top = p->dev_top;
+    a.pop_state = p->dev_pop;
+    a.req_plane = p->dev_plane;
+    a.epoch = p->epoch;
     a.schedule = o.schedule;
     a.total_cost = g.total_cost;
     a.n_units = (int32_t)g.n_units;
@@ -1054,6 +1214,64 @@ cp_status launch_plan(cp_pool *p, const DecodePlan &pl, int32_t n, const int32_t
     ma.n_blocks += g.hq * (int32_t)((uint32_t)g.d_v / merge_block_cols((uint32_t)g.d_v));
   }
   return flush();
+}
+
+// cp_attn_decode_step on a pool with device page stacks: a new token that
+// opens a page takes that page, in every plane, from its model's stack
+// inside the decode launch (fused_append / pop_new_pages). The host only
+// counts: it refills stacks that would run short (a chunk's worth at a
+// time, rarely) and marks the popped entries for reading back at the next
+// slow-path call. A later layer's step finds its plane's entry already in
+// the device page table.
+cp_status step_device_pages(cp_pool *p, const DecodePlan &pl, int32_t n, const int32_t *req_ids,
+                            const int32_t *n_new, const std::vector<int32_t> &placing, const void *rows,
+                            const void *q, void *out, float *lse, void *hip_stream) {
+  const int32_t P = p->st.page_tokens();
+  std::vector<int64_t> need((size_t)p->st.n_models(), 0);
+  std::vector<uint8_t> pops(n, 0);
+  for (int32_t i = 0; i < n; ++i) {
+    const Request &r = p->st.req(req_ids[i]);
+    if (placing[i] && r.ctx_len % P == 0) {
+      pops[i] = 1;
+      need[(size_t)r.model] += r.layers;
+    }
+  }
+  for (int32_t m = 0; m < p->st.n_models(); ++m)
+    if (need[(size_t)m] > kStackCap - kStackRefill)
+      return fail(CP_EINVAL, "a step opens %lld pages of model %d; a device page stack serves at most %d per step",
+                  (long long)need[(size_t)m], m, kStackCap - kStackRefill);
+  DeviceGuard g(p->device);
+  hipStream_t s = (hipStream_t)hip_stream;
+  cp_status rc = refill_stacks(p, need, s);
+  if (rc) return rc;
+  if (++p->epoch >= (1u << 31)) p->epoch = 1;  // pop states hold epoch << 1
+  std::vector<AppendPlan> plan(n);
+  uint64_t off = 0;
+  for (int32_t i = 0; i < n; ++i) {
+    if (!n_new[i]) continue;
+    const Request &r = p->st.req(req_ids[i]);
+    plan[i].flags = kAppRow;
+    plan[i].off = (uint32_t)off;
+    if (pops[i]) {
+      p->st.begin_token_popped(req_ids[i], &p->pending);
+      p->stk[(size_t)r.model].resize(p->stk[(size_t)r.model].size() - (size_t)r.layers);
+      plan[i].flags |= kAppPop;
+      plan[i].pte = (uint32_t)req_ids[i];
+    } else if (placing[i]) {
+      uint64_t first, count;
+      p->st.begin_token(req_ids[i], &first, &count);  // the page exists: nothing to allocate
+    }
+    off += (uint64_t)p->st.model(r.model).row_elems;
+  }
+  rc = launch_plan(p, pl, n, req_ids, q, out, lse, hip_stream, rows, &plan);
+  for (int32_t i = 0; i < n; ++i) p->st.advance(req_ids[i]);
+  if (rc) {
+    // the launch did not run: its pops never happened, so the host's view
+    // of the stacks and page tables is no longer the device's
+    p->broken = true;
+    return rc;
+  }
+  return CP_OK;
 }
 
 // The decode of cp_attn_decode_ex.
@@ -1155,6 +1373,7 @@ cp_status cp_attn_decode_step(cp_pool *p, int32_t n, const int32_t *req_ids, con
     if (rc == CP_OK) advance_all();
     return rc;
   }
+  if (p->dev_pages) return step_device_pages(p, pl, n, req_ids, n_new, placing, rows, q, out, lse, hip_stream);
   rc = prepare_growth(p, n, req_ids, placing.data());
   if (rc) return rc;
 

@@ -96,7 +96,7 @@ __device__ __forceinline__ void mla_unit(const DecodeArgs &a, const GeomK &gm, c
   const int tid = threadIdx.x;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const LaneIds L0 = lane_ids();
-  const int lane = L0.lane, col = L0.col, quad = L0.quad;
+  const int col = L0.col, quad = L0.quad;
   const int P = gm.page_tokens;  // the host routes only pages of a multiple of 32 tokens here
   const int tpp = P / T;
   const int h0 = (int)sg.hblk * C::G;  // first query head of the (single) KV head
@@ -375,7 +375,7 @@ __device__ __forceinline__ void mla_unit(const DecodeArgs &a, const GeomK &gm, c
   // ---- final: score waves publish m and l; every wave normalises its columns
   {
   const LaneIds Lf = lane_ids();
-  const int lane = Lf.lane, col = Lf.col, quad = Lf.quad;
+  const int col = Lf.col, quad = Lf.quad;
   lsum = xor_sum_16_32(lsum);
   __syncthreads();  // every wave is past its last P.V: the rescale records are free
   float *const m_x = reinterpret_cast<float *>(xbuf + C::XFLAGS);

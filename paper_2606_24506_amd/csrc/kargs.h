@@ -13,6 +13,12 @@ constexpr uint32_t kNoWs = 0xFFFFFFFFu;
 // Fixed split workspace of cp_attn_decode_noalloc, per GPU, in bytes.
 constexpr uint64_t kNoAllocScratchBytes = 40ull << 20;
 constexpr int kMaxScratchDevices = 64;
+// Device free-page stacks (pools created with device_pages): entries per
+// model; model m's stack is DecodeArgs::stack[m * kStackCap ...].
+constexpr int32_t kStackCap = 8192;
+// The host refills a stack with up to this many pages (a chunk's worth at
+// most) when a step needs more than it holds.
+constexpr int32_t kStackRefill = 1024;
 enum : int32_t { kSchedBalanced = 0, kSchedQueue = 1, kSchedGrid = 2 };
 // Balanced schedule: the fixed work of one piece (page-table and query
 // loads, the latency of its first pages under a loaded memory system, the
@@ -58,6 +64,8 @@ struct GeomK {
   float scale_log2;    // softmax scale * log2(e)
   int32_t nb;          // head blocks per KV head (vector path)
   int32_t page_cost;   // relative work of one page (balanced schedule)
+  int32_t pool_model;  // the model's id in the pool (its device page stack)
+  int32_t layers;      // KV planes of a request of this model
 };
 
 // One request of a decode launch.
@@ -74,12 +82,14 @@ struct DecReq {
   uint16_t n_chunks;     // KV ranges = partial slots
   uint8_t model;         // index into DecodeArgs::geom
   uint8_t app_flags;     // fused append: kAppRow (the last context token is a new row at
-                         // DecodeArgs::rows + app_off), kAppPage (its page is new: app_pte)
+                         // DecodeArgs::rows + app_off), kAppPage (its page is new: app_pte),
+                         // kAppPop (its page is new and comes from the model's device
+                         // stack, one page per plane; app_pte is then the request id)
   uint16_t n_hblk;       // head blocks per KV range
   uint32_t app_off;      // element offset of the new row in DecodeArgs::rows
   uint32_t app_pte;      // page-table entry of the new row's page when kAppPage is set
 };
-enum : uint8_t { kAppRow = 1, kAppPage = 2 };
+enum : uint8_t { kAppRow = 1, kAppPage = 2, kAppPop = 4 };
 
 struct DecodeArgs {
   uint8_t *pool;          // written only by the fused append
@@ -91,6 +101,14 @@ struct DecodeArgs {
   uint16_t *ws_o;     // partial outputs, [row][d_v] bf16, normalised
   float *ws_l;        // partial log-sum-exp, [row], natural log
   uint32_t *queue;    // queue schedule: {next unit, finished workgroups}
+  // device page stacks (kAppPop): entries and per-model counts, per-request
+  // pop state ((epoch << 1) | done) and page-table entries per plane
+  const uint32_t *stack;
+  int32_t *stack_top;
+  uint32_t *pop_state;
+  const uint32_t *req_plane;
+  uint32_t epoch;  // this launch's pop epoch (>= 1)
+  uint32_t pad0;
   int32_t n_req, n_units;
   int32_t schedule;     // kSchedBalanced, kSchedQueue or kSchedGrid
   uint32_t total_cost;  // balanced: summed page costs of the launch
@@ -144,7 +162,19 @@ struct GatherArgs {
   GeomK geom;
 };
 
+// Refill of a device page stack: n entries written at dst[0..n), then the
+// model's count set to new_top. The entries travel in the arguments, so the
+// host keeps no staging copy alive.
+constexpr int32_t kStackPushMax = 640;
+struct StackPushArgs {
+  uint32_t *dst;
+  int32_t *top;
+  int32_t n, new_top;
+  uint32_t ent[kStackPushMax];
+};
+
 static_assert(kMaxReqPerLaunch <= 64, "request lookups search one key per lane");
+static_assert(sizeof(StackPushArgs) <= 3072, "stack push arguments too large");
 static_assert(sizeof(DecodeArgs) <= 3584, "decode kernel arguments too large");
 static_assert(sizeof(MergeArgs) <= 3072, "merge kernel arguments too large");
 static_assert(sizeof(AppendArgs) <= 3072, "append kernel arguments too large");

@@ -48,6 +48,18 @@ hipError_t launch_append(const AppendArgs &a, hipStream_t stream) {
   return hipGetLastError();
 }
 
+// ------------------------------------------------- device page stacks
+
+__global__ __launch_bounds__(256) void stack_push_kernel(const StackPushArgs a) {
+  for (int32_t i = threadIdx.x; i < a.n; i += blockDim.x) a.dst[i] = a.ent[i];
+  if (threadIdx.x == 0) *a.top = a.new_top;
+}
+
+hipError_t launch_stack_push(const StackPushArgs &a, hipStream_t stream) {
+  hipLaunchKernelGGL(stack_push_kernel, dim3(1), dim3(256), 0, stream, a);
+  return hipGetLastError();
+}
+
 // ------------------------------------------------------------- gather
 
 __global__ __launch_bounds__(256) void kv_gather_kernel(const GatherArgs a) {

@@ -277,6 +277,31 @@ void PoolState::begin_token(int32_t id, uint64_t *first, uint64_t *count) {
   r.inflight = 1;
 }
 
+void PoolState::take_pages(int32_t model, int64_t k, std::vector<uint32_t> *out) {
+  for (int64_t i = 0; i < k; ++i) out->push_back(alloc_page(model));
+  acct_[model].in_stack += k;
+}
+
+void PoolState::return_pages(const std::vector<uint32_t> &ptes) {
+  for (uint32_t pte : ptes) {
+    const int32_t model = chunks_[(size_t)(((uint64_t)pte << 8) / chunk_bytes_)].model;
+    acct_[model].in_stack -= 1;
+    free_page(pte);
+  }
+}
+
+void PoolState::begin_token_popped(int32_t id, std::vector<uint64_t> *slots) {
+  Request &r = reqs_[id];
+  for (int32_t l = 0; l < r.layers; ++l) {
+    const uint64_t slot = r.plane_base(l) + (uint64_t)r.pages_used;
+    pte_[slot] = kPendingPte;
+    slots->push_back(slot);
+  }
+  r.pages_used += 1;
+  r.inflight = 1;
+  acct_[r.model].in_stack -= r.layers;
+}
+
 void PoolState::advance(int32_t id) {
   Request &r = reqs_[id];
   if (++r.cursor == r.layers) {
@@ -436,7 +461,7 @@ void PoolState::trim(int32_t model) {
 
 uint64_t PoolState::pages_used() const {
   uint64_t t = 0;
-  for (auto &a : acct_) t += (uint64_t)a.used;
+  for (auto &a : acct_) t += (uint64_t)(a.used - a.in_stack);
   return t;
 }
 

@@ -30,6 +30,10 @@ namespace cp {
 
 enum Kind : int32_t { kMLA = 0, kGQA = 1 };
 
+// Mirror value of a page-table entry written by the device and not yet read
+// back (device page stacks).
+constexpr uint32_t kPendingPte = 0xFFFFFFFFu;
+
 struct Geom {
   int32_t kind = 0;
   int32_t hq = 0, hkv = 0, g = 0;  // g = query heads per KV head
@@ -156,6 +160,23 @@ class PoolState {
   // Returns chunks of *carved that hold no pages to the free list.
   void release_empty(const std::vector<int32_t> &carved);
 
+  // Device page stacks (pools whose decode steps take new pages on the
+  // device). Pages handed to a model's stack are allocated (they count
+  // against the model's reservations) but belong to no request until a
+  // step pops them.
+  // Pages the model may still hand out: its reservations minus its
+  // allocated pages.
+  int64_t stack_room(int32_t model) const { return acct_[model].reserved - acct_[model].used; }
+  int64_t in_stack(int32_t model) const { return acct_[model].in_stack; }
+  // Allocates k pages for the model's stack (after ensure_slots).
+  void take_pages(int32_t model, int64_t k, std::vector<uint32_t> *out);
+  // Frees pages taken back from a stack.
+  void return_pages(const std::vector<uint32_t> &ptes);
+  // Places a new token that opens a page in every plane, the pages being
+  // popped from the model's device stack by the step: their entries stay
+  // kPendingPte in the mirror until read back. Appends the entries' slots.
+  void begin_token_popped(int32_t id, std::vector<uint64_t> *slots);
+
   const uint32_t *pte_mirror() const { return pte_.data(); }
   uint32_t *pte_mirror_mut() { return pte_.data(); }
 
@@ -176,6 +197,7 @@ class PoolState {
     int64_t reserved = 0;   // pages promised to open requests
     int64_t used = 0;       // pages holding KV
     int64_t held = 0;       // chunks carved for this model
+    int64_t in_stack = 0;   // allocated pages held by the model's device stack
     std::map<int32_t, int32_t> partial;  // chunk -> free slots (chunks with room)
   };
 

@@ -53,20 +53,54 @@ __device__ __forceinline__ int unit_segment(const DecodeArgs &a, uint32_t u, Seg
   return r;
 }
 
+// Device page stack (kAppPop; run by one thread): the first piece of this
+// launch to reach request rq's new page claims the request's pop, takes one
+// page per KV plane from the top of the model's stack and writes their
+// page-table entries (plane l gets the entry l below the top); any other
+// piece waits until the claimant has published them. The claimant waits on
+// nothing, so every wait ends. Returns the entry of the new page of the
+// plane rq attends over.
+__device__ __forceinline__ uint32_t pop_new_pages(const DecodeArgs &a, const DecReq &rq, uint32_t pg) {
+  const GeomK &g = a.geom[rq.model];
+  const uint32_t rid = rq.app_pte;
+  uint32_t *st = a.pop_state + rid;
+  const uint32_t claim = a.epoch << 1, done = claim | 1u;
+  uint32_t s = __hip_atomic_load(st, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT);
+  if (s != done) {
+    if (s != claim && atomicCAS(st, s, claim) == s) {
+      const int32_t L = g.layers;
+      const uint32_t plane = a.req_plane[rid];
+      const int32_t top = atomicSub(&a.stack_top[g.pool_model], L);
+      const uint32_t *stk = a.stack + (uint64_t)g.pool_model * kStackCap;
+      for (int32_t l = 0; l < L; ++l) a.pte[rq.pte_base + (uint32_t)l * plane + pg] = stk[top - 1 - l];
+      __hip_atomic_store(st, done, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+    } else {
+      while (__hip_atomic_load(st, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT) != done) __builtin_amdgcn_s_sleep(1);
+    }
+  }
+  return __hip_atomic_load(a.pte + rq.pte_base + pg, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 // Fused append (cp_attn_decode_step): every piece whose page range holds a
 // request's last context token, when that token is new in this call, first
-// writes the page-table entry of a newly allocated page and copies the new
-// logical row into its page; then the piece reads the page as usual. When
-// several pieces (head blocks) cover that page they all write the same
-// bytes, which is harmless; each one's own stores precede its loads through
-// the workgroup barrier.
+// writes the page-table entry of a newly allocated page (taken from the
+// launch arguments, or popped from the model's device stack) and copies
+// the new logical row into its page; then the piece reads the page as
+// usual. When several pieces (head blocks) cover that page they all write
+// the same bytes, which is harmless; each one's own stores precede its
+// loads through the workgroup barrier.
 __device__ __forceinline__ void fused_append(const DecodeArgs &a, const DecReq &rq, const Seg &sg) {
   const GeomK &g = a.geom[rq.model];
   const uint32_t P = (uint32_t)g.page_tokens;
   const uint32_t pos = rq.ctx_len - 1, pg = pos / P;
   if (pg < sg.pg_begin || pg >= sg.pg_end) return;
   uint32_t pte;
-  if (rq.app_flags & kAppPage) {
+  if (rq.app_flags & kAppPop) {
+    __shared__ uint32_t popped;
+    if (threadIdx.x == 0) popped = pop_new_pages(a, rq, pg);
+    __syncthreads();
+    pte = popped;
+  } else if (rq.app_flags & kAppPage) {
     pte = rq.app_pte;
     if (threadIdx.x == 0) a.pte[rq.pte_base + pg] = pte;
   } else {

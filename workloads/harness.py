@@ -58,7 +58,7 @@ def to_device_u16(arr: np.ndarray, device):
 def load(wl: Workload, device: int = 0, *, placement_seed: Optional[int] = None, reserve_extra: int = 0,
          interleave: int = 0, rows_override: Optional[Dict[int, np.ndarray]] = None,
          q_override: Optional[List[np.ndarray]] = None, chunk_rows: int = 1 << 17, backing: int = 0,
-         n_layers: int = 1) -> Loaded:
+         n_layers: int = 1, device_pages: int = 0) -> Loaded:
     """Build a pool holding the workload.
 
     interleave > 0 appends rows in rounds of `interleave` tokens per request,
@@ -66,7 +66,8 @@ def load(wl: Workload, device: int = 0, *, placement_seed: Optional[int] = None,
     request index to its rows (uint16 bits) instead of the seeded draw.
     backing selects the pool's memory (0 one buffer, 1 virtual ranges).
     n_layers > 1 registers the models with that many KV planes, each holding
-    the same rows.
+    the same rows. device_pages = 1 gives the models device free-page stacks
+    (decode steps take new pages on the device).
     """
     import torch
 
@@ -75,7 +76,7 @@ def load(wl: Workload, device: int = 0, *, placement_seed: Optional[int] = None,
     dev = torch.device("cuda", device)
     seed = wl.placement_seed if placement_seed is None else placement_seed
     pool = cpl.Pool(page_tokens=PAGE_TOKENS, pool_bytes=wl.pool_bytes, chunk_bytes=wl.chunk_bytes,
-                    placement_seed=seed, device=device, backing=backing)
+                    placement_seed=seed, device=device, backing=backing, device_pages=device_pages)
     mids = {name: pool.register_spec(MODELS[name], n_layers=n_layers) for name in wl.models_used()}
     if wl.filler_model and wl.filler_model not in mids:
         mids[wl.filler_model] = pool.register_spec(MODELS[wl.filler_model], n_layers=n_layers)
