@@ -76,6 +76,10 @@ def parse():
     ap.add_argument("--planes", action="store_true",
                     help="one pool whose models have one KV plane per layer, the steps moving each request's "
                          "layer cursor, instead of one pool per layer")
+    ap.add_argument("--layer-launch", type=int, default=0, metavar="L",
+                    help="also time steps that take every request through L KV layers in one "
+                         "cp_attn_decode_layers call, against L per-layer cp_attn_decode_step calls on the same pool "
+                         "(reported under layer_launch)")
     ap.add_argument("--device-pages", action="store_true",
                     help="pools with device free-page stacks: the steps pop new pages inside the launch")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -382,6 +386,69 @@ def measure(cfg: int, args) -> dict:
     return rec
 
 
+def measure_layer_launch(cfg: int, args) -> dict:
+    """One pool whose models have L KV planes; a step takes one new token
+    per request through all L layers, either as L per-layer
+    cp_attn_decode_step calls (the host moving the layer cursors) or as one
+    cp_attn_decode_layers call (the launch moving them). Same queries and
+    rows for every layer (timing only). Returns both records."""
+    import torch
+
+    from workloads import make_workload
+    from workloads.harness import load, to_device_u16
+
+    L = args.layer_launch
+    wl = make_workload(cfg, scale_ctx=args.ctx_scale)
+    if wl.filler_pages:
+        sys.exit("--layer-launch: the filler requests of this pool leave no room for more KV planes")
+    B = len(wl.requests)
+    steps, warm = args.steps, args.warmup
+    ld = load(wl, reserve_extra=2 * (warm + 2 * steps) + 4, n_layers=L, device_pages=int(args.device_pages))
+    hq = [wl.model(r).n_q_heads for r in range(B)]
+    qd = [wl.model(r).d_k for r in range(B)]
+    dv = [wl.model(r).d_v for r in range(B)]
+    q1 = ld.q
+    qL = torch.cat([q1[sum(h * d for h, d in zip(hq[:r], qd[:r])):][:hq[r] * qd[r]].repeat(L) for r in range(B)])
+    outL = torch.empty(L * sum(h * d for h, d in zip(hq, dv)), dtype=torch.int16, device="cuda")
+    lseL = torch.empty(L * sum(hq), dtype=torch.float32, device="cuda")
+    row1 = [wl.step_rows_bits(r, 0).reshape(-1) for r in range(B)]
+    rows1 = to_device_u16(np.concatenate(row1), "cuda")
+    rowsL = to_device_u16(np.concatenate([np.tile(x, L) for x in row1]), "cuda")
+    ones = [1] * B
+    stream = torch.cuda.current_stream()
+
+    def per_layer():
+        for _ in range(L):
+            ld.pool.decode_step(ld.req_ids, ones, rows1, q1, ld.out, ld.lse, stream)
+
+    def one_call():
+        ld.pool.decode_layers(ld.req_ids, ones, rowsL, qL, outL, lseL, stream)
+
+    rec = {}
+    for name, fn in (("per_layer_steps", per_layer), ("one_launch", one_call)):
+        for _ in range(warm):
+            fn()
+        torch.cuda.synchronize()
+        ctx = [ld.pool.ctx_len(r) for r in ld.req_ids]
+        t0 = time.perf_counter()
+        for _ in range(steps):
+            fn()
+        t_enq = time.perf_counter() - t0
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        by = sum(L * algorithmic_bytes_decode(wl, [c + 1 + i for c in ctx]) for i in range(steps))
+        rec[name] = {"ms_per_token_step": round(wall * 1e3 / steps, 5),
+                     "host_enqueue_ms_per_token_step": round(t_enq * 1e3 / steps, 5),
+                     "decode_GBps": round(by / wall / 1e9, 2),
+                     "frac_of_peak": round(by / wall / 1e9 / HBM_PEAK_GBS, 4)}
+        log(f"cfg{cfg} x {L} layers, {name}: {rec[name]}")
+    ld.close()
+    torch.cuda.empty_cache()
+    return {"workload": WORKLOAD_NAMES[cfg], "layers": L,
+            "step": "one new token per request through every layer: L cp_attn_decode_step calls, or one "
+                    "cp_attn_decode_layers call", **rec}
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -432,6 +499,8 @@ def main():
         "matrix": head["matrix"],
         "per_config": per_config,
     }
+    if args.layer_launch:
+        res["layer_launch"] = measure_layer_launch(2 if args.config == 3 else args.config, args)
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(make_workload(args.config), args.cpu_seconds)
     print(json.dumps(res))

@@ -388,14 +388,56 @@ cp_status cp_attn_decode_noalloc(cp_pool *pool, int32_t n, const int32_t *req_id
  * flight (its row of that layer) and 0 otherwise. The token is committed
  * after the last layer's step. A single-layer model commits at once, which
  * is the behaviour described above.
+ * With device_pages (cp_pool_desc), a new token's pages are popped from the
+ * model's device stack inside the launch instead (all planes at the first
+ * layer's step).
  * Errors: those of cp_kv_append and cp_attn_decode_ex, plus CP_EINVAL for an
  * n_new other than 0 or 1 or not matching the token in flight. Argument and
  * capacity checks run before any state changes; if the attention launch
  * fails once pages are allocated, the rows are still appended (as by
- * cp_kv_append), the cursors move on, and the error is returned. */
+ * cp_kv_append), the cursors move on, and the error is returned (with
+ * device_pages the pool is then unusable: later calls return CP_ESTATE). */
 cp_status cp_attn_decode_step(cp_pool *pool, int32_t n, const int32_t *req_ids, const int32_t *n_new,
                               const void *rows, const void *q, void *out, float *lse, void *hip_stream,
                               const cp_decode_opts *opts);
+
+/* One token step through every KV layer of the requests' models in one
+ * planned call (Section 3.2, layer-wise pipeline: the layer cursor of each
+ * in-flight request is advanced by the launch itself as its layers
+ * complete). For each request i and layer l in [0, n_layers(i)) it has the
+ * effect of a cp_attn_decode_step at layer l with that layer's query and
+ * row, with the same results bit for bit; the work of all layers is spread
+ * over one launch per kernel family (KV planes of different layers are
+ * independent inputs here: the FFN stage between layers is outside this
+ * library).
+ *
+ *   n_new  host, n entries, each 0 or 1; every request must be at layer 0
+ *          with no token in flight (CP_ESTATE otherwise).
+ *   rows   device, bf16; for each request with n_new = 1, in call order,
+ *          its new token's rows of every layer: [n_layers][row_elems].
+ *   q      device, bf16: per request in call order, [n_layers][n_q_heads]
+ *          [d_k]; out [n_layers][n_q_heads][d_v] and lse [n_layers]
+ *          [n_q_heads] likewise.
+ *
+ * On the device, the last piece of work of each (request, layer) moves the
+ * request's layer cursor on; the one that completes the last layer sets it
+ * back to 0 and counts the new token as carried through every layer
+ * (cp_request_layer_state). On the host the token is committed when the
+ * call returns. New pages come from the host allocator, or from the device
+ * stacks (device_pages: one pop per request covers every plane). Errors: as
+ * cp_attn_decode_step; the per-request limits of an all-layer launch are
+ * request ids below 2^20 and fewer than 4096 layers. If the launch fails
+ * after pages were allocated, the pool is unusable (CP_ESTATE). */
+cp_status cp_attn_decode_layers(cp_pool *pool, int32_t n, const int32_t *req_ids, const int32_t *n_new,
+                                const void *rows, const void *q, void *out, float *lse, void *hip_stream,
+                                const cp_decode_opts *opts);
+
+/* The device-side layer state that cp_attn_decode_layers launches drive:
+ * the layer cursor (layers of the current all-layer step completed; 0 when
+ * none is running) and the tokens carried through every layer since the
+ * request was opened. Waits for the device. For tests and monitoring.
+ * Errors: CP_EINVAL, CP_ESTATE (host-only pool), CP_EHIP. */
+cp_status cp_request_layer_state(cp_pool *pool, int32_t req_id, int32_t *layer, int64_t *tokens);
 
 /* Copy logical rows [start, start + n_tok) of one request out of the pool
  * into dst (device, [n_layers][n_tok][row_elems] bf16), through the same

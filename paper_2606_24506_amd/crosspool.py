@@ -145,6 +145,9 @@ def _load() -> C.CDLL:
         "cp_attn_decode_noalloc": ([P, I32, C.POINTER(I32), VP, VP, VP, VP, C.POINTER(cp_decode_opts)], I32),
         "cp_attn_decode_step": ([P, I32, C.POINTER(I32), C.POINTER(I32), VP, VP, VP, VP, VP, C.POINTER(cp_decode_opts)],
                                 I32),
+        "cp_attn_decode_layers": ([P, I32, C.POINTER(I32), C.POINTER(I32), VP, VP, VP, VP, VP,
+                                   C.POINTER(cp_decode_opts)], I32),
+        "cp_request_layer_state": ([P, I32, C.POINTER(I32), C.POINTER(I64)], I32),
         "cp_kv_gather": ([P, I32, I64, I64, VP, VP], I32),
         "cp_plan_pool": ([C.POINTER(cp_plan_model), I32, C.POINTER(cp_plan_opts), C.POINTER(cp_plan_result)], I32),
     }
@@ -314,6 +317,26 @@ def cp_attn_decode_step(pool: int, req_ids: Sequence[int], n_new: Sequence[int],
                                    _ptr(lse), _stream(stream), C.byref(o)))
 
 
+def cp_attn_decode_layers(pool: int, req_ids: Sequence[int], n_new: Sequence[int], rows, q, out, lse, stream=None, *,
+                          num_splits: int = 0, schedule: int = CP_SCHED_BALANCED, path: int = CP_PATH_AUTO,
+                          ev_begin=None, ev_end=None) -> None:
+    def ev(e):
+        if e is None:
+            return None
+        return e.cuda_event if hasattr(e, "cuda_event") else int(e)
+
+    o = cp_decode_opts(num_splits, schedule, path, 0, ev(ev_begin), ev(ev_end))
+    n = len(req_ids)
+    _check(LIB.cp_attn_decode_layers(pool, n, _i32_array(req_ids), _i32_array(n_new), _ptr(rows), _ptr(q), _ptr(out),
+                                     _ptr(lse), _stream(stream), C.byref(o)))
+
+
+def cp_request_layer_state(pool: int, req_id: int):
+    layer, tokens = C.c_int32(), C.c_int64()
+    _check(LIB.cp_request_layer_state(pool, req_id, C.byref(layer), C.byref(tokens)))
+    return layer.value, tokens.value
+
+
 def cp_kv_gather(pool: int, req_id: int, start: int, n_tok: int, dst, stream=None) -> None:
     _check(LIB.cp_kv_gather(pool, req_id, start, n_tok, _ptr(dst), _stream(stream)))
 
@@ -396,6 +419,12 @@ class Pool:
 
     def decode_step(self, req_ids, n_new, rows, q, out, lse, stream=None, **opts) -> None:
         cp_attn_decode_step(self.handle, req_ids, n_new, rows, q, out, lse, stream, **opts)
+
+    def decode_layers(self, req_ids, n_new, rows, q, out, lse, stream=None, **opts) -> None:
+        cp_attn_decode_layers(self.handle, req_ids, n_new, rows, q, out, lse, stream, **opts)
+
+    def layer_state(self, req_id: int):
+        return cp_request_layer_state(self.handle, req_id)
 
     def gather(self, req_id, start, n_tok, dst, stream=None) -> None:
         cp_kv_gather(self.handle, req_id, start, n_tok, dst, stream)

@@ -113,10 +113,15 @@ struct cp_pool {
   uint32_t *dev_stack = nullptr;
   int32_t *dev_top = nullptr;
   uint32_t *dev_pop = nullptr;
-  uint32_t *dev_plane = nullptr;
+  uint32_t *dev_geo = nullptr;  // per request id: {first page-table entry, entries per plane}
   uint32_t epoch = 0;
   std::vector<std::vector<uint32_t>> stk;
   std::vector<uint64_t> pending;
+  // All-layer launches: per request id its layer cursor and the tokens
+  // carried through every layer ([2 id], [2 id + 1]); per launch entry the
+  // pieces finished.
+  uint32_t *dev_layer = nullptr;
+  uint32_t *dev_entry = nullptr;
 };
 
 namespace {
@@ -391,10 +396,16 @@ cp_status cp_pool_create(const cp_pool_desc *d, cp_pool **out) {
       ok = hipMalloc((void **)&p->dev_stack, nm * kStackCap * 4) == hipSuccess &&
            hipMalloc((void **)&p->dev_top, nm * 4) == hipSuccess &&
            hipMalloc((void **)&p->dev_pop, nr * 4) == hipSuccess &&
-           hipMalloc((void **)&p->dev_plane, nr * 4) == hipSuccess;
+           hipMalloc((void **)&p->dev_geo, nr * 8) == hipSuccess;
       if (ok)
         ok = hipMemset(p->dev_top, 0, nm * 4) == hipSuccess && hipMemset(p->dev_pop, 0, nr * 4) == hipSuccess &&
-             hipMemset(p->dev_plane, 0, nr * 4) == hipSuccess;
+             hipMemset(p->dev_geo, 0, nr * 8) == hipSuccess;
+    }
+    if (ok) {
+      const uint64_t nr = (uint64_t)p->st.max_requests();
+      ok = hipMalloc((void **)&p->dev_layer, nr * 8) == hipSuccess &&
+           hipMalloc((void **)&p->dev_entry, kMaxReqPerLaunch * 4) == hipSuccess;
+      if (ok) ok = hipMemset(p->dev_layer, 0, nr * 8) == hipSuccess && hipMemset(p->dev_entry, 0, kMaxReqPerLaunch * 4) == hipSuccess;
     }
     if (ok) std::memset(p->pin_pte, 0, nptes * 4);
     int cus = 0;
@@ -427,7 +438,8 @@ cp_status cp_pool_destroy(cp_pool *p) {
     if (p->dev_pte) (void)hipFree(p->dev_pte);
     if (p->pin_pte) (void)hipHostFree(p->pin_pte);
     if (p->queue) (void)hipFree(p->queue);
-    for (void *b : {(void *)p->dev_stack, (void *)p->dev_top, (void *)p->dev_pop, (void *)p->dev_plane})
+    for (void *b : {(void *)p->dev_stack, (void *)p->dev_top, (void *)p->dev_pop, (void *)p->dev_geo,
+                    (void *)p->dev_layer, (void *)p->dev_entry})
       if (b) (void)hipFree(b);
     if (p->ws_o) (void)hipFree(p->ws_o);
     if (p->ws_l) (void)hipFree(p->ws_l);
@@ -489,14 +501,16 @@ cp_status cp_request_open(cp_pool *p, int32_t model_id, int64_t reserve_tokens, 
   if (rc == -3) return fail(CP_ENOSPC, "%s", err.c_str());
   if (rc == -2) return fail(CP_ENOMEM, "%s", err.c_str());
   if (rc != 0) return fail(CP_EINVAL, "%s", err.c_str());
-  if (p->dev_pages && !p->host_only) {
-    // the plane stride the device pops use for this request id
+  if (!p->host_only) {
+    // the page-table geometry the device pops use, and a fresh layer cursor
     DeviceGuard g(p->device);
-    const uint32_t plane = (uint32_t)p->st.req(*req_id).plane;
-    hipError_t e = hipMemcpy(p->dev_plane + *req_id, &plane, 4, hipMemcpyHostToDevice);
+    const Request &r = p->st.req(*req_id);
+    const uint32_t geo[2] = {r.pte_base, (uint32_t)r.plane}, zero[2] = {0u, 0u};
+    hipError_t e = hipMemcpy(p->dev_layer + 2 * (uint64_t)*req_id, zero, 8, hipMemcpyHostToDevice);
+    if (e == hipSuccess && p->dev_pages) e = hipMemcpy(p->dev_geo + 2 * (uint64_t)*req_id, geo, 8, hipMemcpyHostToDevice);
     if (e != hipSuccess) {
       p->st.close(*req_id);
-      return hip_fail(e, "recording the request's plane stride");
+      return hip_fail(e, "initialising the request's device state");
     }
   }
   return CP_OK;
@@ -1123,7 +1137,8 @@ cp_status bind_pool_workspace(cp_pool *p, DecodePlan *pl) {
 // cp_attn_decode_step) and the merges of split requests. Only HIP failures
 // remain possible here.
 cp_status launch_plan(cp_pool *p, const DecodePlan &pl, int32_t n, const int32_t *req_ids, const void *q,
-                      void *out, float *lse, void *hip_stream, const void *rows, const std::vector<AppendPlan> *app) {
+                      void *out, float *lse, void *hip_stream, const void *rows, const std::vector<AppendPlan> *app,
+                      const int32_t *layer = nullptr, const uint32_t *tag = nullptr) {
   const cp_decode_opts &o = pl.o;
   DeviceGuard dg(p->device);
   hipStream_t s = (hipStream_t)hip_stream;
@@ -1145,8 +1160,11 @@ cp_status launch_plan(cp_pool *p, const DecodePlan &pl, int32_t n, const int32_t
     a.stack = p->dev_stack;
     a.stack_top = p->dev_top;
     a.pop_state = p->dev_pop;
-    a.req_plane = p->dev_plane;
+    a.req_geo = p->dev_geo;
     a.epoch = p->epoch;
+    a.layer_cursor = p->dev_layer;
+    a.layer_tokens = p->dev_layer + 1;  // indexed by 2 * request id below
+    a.entry_done = p->dev_entry;
     a.schedule = o.schedule;
     a.total_cost = g.total_cost;
     a.n_units = (int32_t)g.n_units;
@@ -1154,7 +1172,9 @@ cp_status launch_plan(cp_pool *p, const DecodePlan &pl, int32_t n, const int32_t
     for (int32_t i : g.idx) {
       const Request &r = p->st.req(req_ids[i]);
       DecReq &d = a.req[a.n_req++];
-      d.pte_base = r.plane_base(r.cursor);  // the KV plane of the request's current layer
+      // the KV plane of the entry's layer, or of the request's current layer
+      d.pte_base = r.plane_base(layer ? layer[i] : r.cursor);
+      a.ent_tag[a.n_req - 1] = tag ? tag[i] : 0u;
       d.ctx_len = (uint32_t)pl.attend[i];
       d.q_off = (uint32_t)pl.q_off[i];
       d.o_off = (uint32_t)pl.o_off[i];
@@ -1274,6 +1294,129 @@ cp_status step_device_pages(cp_pool *p, const DecodePlan &pl, int32_t n, const i
   return CP_OK;
 }
 
+// cp_attn_decode_layers: every KV layer of every request in one planned
+// call. Launch entries are (request, layer) pairs, request-major, so the
+// packed query, output and lse offsets the planner computes are [request]
+// [layer][head] ones; entry (i, l) attends over plane l, and its last piece
+// moves request i's device layer cursor on (piece_done).
+cp_status decode_layers_impl(cp_pool *p, int32_t n, const int32_t *req_ids, const int32_t *n_new, const void *rows,
+                             const void *q, void *out, float *lse, void *hip_stream, const cp_decode_opts *opts) {
+  DecodePlan pl;
+  cp_status rc = decode_prepare(p, n, req_ids, q, out, lse, opts, &pl.o, &pl.gk);
+  if (rc) return rc;
+  if (!n_new) return fail(CP_EINVAL, "null n_new");
+  int64_t entries = 0;
+  bool any = false;
+  for (int32_t i = 0; i < n; ++i) {
+    const Request &r = p->st.req(req_ids[i]);
+    if (r.cursor != 0 || r.inflight)
+      return fail(CP_ESTATE, "request %d has a token in flight at layer %d; finish it with cp_attn_decode_step first",
+                  req_ids[i], r.cursor);
+    if (n_new[i] != 0 && n_new[i] != 1)
+      return fail(CP_EINVAL, "cp_attn_decode_layers appends 0 or 1 tokens per request (request %d: %d)", req_ids[i],
+                  n_new[i]);
+    if (r.ctx_len + n_new[i] < 1) return fail(CP_EINVAL, "request %d has an empty context", req_ids[i]);
+    if (r.ctx_len + n_new[i] > 0xFFFFFFF0ll) return fail(CP_EINVAL, "context length overflow");
+    if (!p->st.fits_reservation(req_ids[i], r.ctx_len + n_new[i]))
+      return fail(CP_EINVAL, "request %d would grow past its reservation of %lld pages", req_ids[i],
+                  (long long)r.reserve_pages);
+    if ((uint32_t)req_ids[i] >= (1u << kTagLayerShift) || r.layers >= (1 << (32 - kTagLayerShift)))
+      return fail(CP_EINVAL, "request id or layer count too large for an all-layer launch");
+    entries += r.layers;
+    any = any || n_new[i] != 0;
+  }
+  if (any && !rows) return fail(CP_EINVAL, "null rows");
+  if (entries > (1 << 20)) return fail(CP_EINVAL, "too many (request, layer) entries in one call");
+  const int32_t E = (int32_t)entries;
+  std::vector<int32_t> eid(E), elayer(E), extra(E);
+  std::vector<uint32_t> etag(E);
+  uint64_t total_elems = 0;
+  for (int32_t i = 0, k = 0; i < n; ++i) {
+    const Request &r = p->st.req(req_ids[i]);
+    for (int32_t l = 0; l < r.layers; ++l, ++k) {
+      eid[k] = req_ids[i];
+      elayer[k] = l;
+      extra[k] = n_new[i];
+      etag[k] = (uint32_t)req_ids[i] | ((uint32_t)r.layers << kTagLayerShift);
+    }
+    if (n_new[i]) total_elems += (uint64_t)r.layers * (uint64_t)p->st.model(r.model).row_elems;
+  }
+  if (total_elems > 0xFFFFFFFFull) return fail(CP_EINVAL, "too many rows in one call");
+  rc = plan_decode(p, E, eid.data(), extra.data(), &pl);
+  if (rc) return rc;
+  rc = bind_pool_workspace(p, &pl);
+  if (rc) return rc;
+  DeviceGuard g(p->device);
+  hipStream_t s = (hipStream_t)hip_stream;
+  if (!any) return launch_plan(p, pl, E, eid.data(), q, out, lse, hip_stream, nullptr, nullptr, elayer.data(), etag.data());
+
+  // New tokens: pages of every plane, from the host allocator (their
+  // entries travel with the launch, one per entry) or from the device
+  // stacks (one claim per request pops them all).
+  const int32_t P = p->st.page_tokens();
+  std::vector<uint8_t> opens(n, 0);
+  std::vector<int64_t> need((size_t)p->st.n_models(), 0);
+  for (int32_t i = 0; i < n; ++i) {
+    const Request &r = p->st.req(req_ids[i]);
+    if (n_new[i] && r.ctx_len % P == 0) {
+      opens[i] = 1;
+      need[(size_t)r.model] += r.layers;
+    }
+  }
+  if (p->dev_pages) {
+    for (int32_t m = 0; m < p->st.n_models(); ++m)
+      if (need[(size_t)m] > kStackCap - kStackRefill)
+        return fail(CP_EINVAL, "a call opens %lld pages of model %d; a device page stack serves at most %d per call",
+                    (long long)need[(size_t)m], m, kStackCap - kStackRefill);
+    rc = refill_stacks(p, need, s);
+    if (rc) return rc;
+    if (++p->epoch >= (1u << 31)) p->epoch = 1;
+  } else {
+    rc = prepare_growth(p, n, req_ids, n_new);
+    if (rc) return rc;
+  }
+  std::vector<AppendPlan> plan(E);
+  uint64_t off = 0;
+  for (int32_t i = 0, k = 0; i < n; ++i) {
+    const Request &r = p->st.req(req_ids[i]);
+    const int32_t L = r.layers;
+    const uint32_t row = (uint32_t)p->st.model(r.model).row_elems;
+    const uint64_t pg = (uint64_t)(r.ctx_len / P);  // the new token's page
+    if (!n_new[i]) {
+      k += L;
+      continue;
+    }
+    if (opens[i] && p->dev_pages) {
+      p->st.begin_token_popped(req_ids[i], &p->pending);
+      p->stk[(size_t)r.model].resize(p->stk[(size_t)r.model].size() - (size_t)L);
+    } else {
+      uint64_t first, count;
+      p->st.begin_token(req_ids[i], &first, &count);
+    }
+    for (int32_t l = 0; l < L; ++l, ++k) {
+      plan[k].flags = kAppRow;
+      plan[k].off = (uint32_t)(off + (uint64_t)l * row);
+      if (opens[i] && p->dev_pages) {
+        plan[k].flags |= kAppPop;
+        plan[k].pte = (uint32_t)req_ids[i];
+      } else if (opens[i]) {
+        plan[k].flags |= kAppPage;
+        plan[k].pte = p->st.pte_mirror()[r.plane_base(l) + pg];
+      }
+    }
+    off += (uint64_t)L * row;
+  }
+  rc = launch_plan(p, pl, E, eid.data(), q, out, lse, hip_stream, rows, &plan, elayer.data(), etag.data());
+  for (int32_t i = 0; i < n; ++i) p->st.commit_token(req_ids[i]);
+  if (rc) {
+    // the launch did not run: its rows, and any popped page entries, are
+    // missing on the device
+    p->broken = true;
+    return rc;
+  }
+  return CP_OK;
+}
+
 // The decode of cp_attn_decode_ex.
 cp_status decode_impl(cp_pool *p, int32_t n, const int32_t *req_ids, const void *q, void *out, float *lse,
                       void *hip_stream, const cp_decode_opts *opts) {
@@ -1320,6 +1463,25 @@ cp_status cp_attn_decode_noalloc(cp_pool *p, int32_t n, const int32_t *req_ids, 
     pl.ws_l = reinterpret_cast<float *>(static_cast<uint8_t *>(base) + o_bytes);
   }
   return launch_plan(p, pl, n, req_ids, q, out, lse, hip_stream, nullptr, nullptr);
+}
+
+cp_status cp_attn_decode_layers(cp_pool *p, int32_t n, const int32_t *req_ids, const int32_t *n_new, const void *rows,
+                                const void *q, void *out, float *lse, void *hip_stream, const cp_decode_opts *opts) {
+  return decode_layers_impl(p, n, req_ids, n_new, rows, q, out, lse, hip_stream, opts);
+}
+
+cp_status cp_request_layer_state(cp_pool *p, int32_t req_id, int32_t *layer, int64_t *tokens) {
+  if (!p || !layer || !tokens) return fail(CP_EINVAL, "null argument");
+  if (!p->st.valid_open(req_id)) return fail(CP_EINVAL, "request %d is not open", req_id);
+  if (p->host_only) return fail(CP_ESTATE, "host-only pool has no device state");
+  DeviceGuard g(p->device);
+  hipError_t e = hipDeviceSynchronize();
+  uint32_t v[2] = {0u, 0u};
+  if (e == hipSuccess) e = hipMemcpy(v, p->dev_layer + 2 * (uint64_t)req_id, 8, hipMemcpyDeviceToHost);
+  if (e != hipSuccess) return hip_fail(e, "reading the request's layer cursor");
+  *layer = (int32_t)v[0];
+  *tokens = (int64_t)v[1];
+  return CP_OK;
 }
 
 cp_status cp_attn_decode_step(cp_pool *p, int32_t n, const int32_t *req_ids, const int32_t *n_new, const void *rows,

@@ -102,19 +102,30 @@ struct DecodeArgs {
   float *ws_l;        // partial log-sum-exp, [row], natural log
   uint32_t *queue;    // queue schedule: {next unit, finished workgroups}
   // device page stacks (kAppPop): entries and per-model counts, per-request
-  // pop state ((epoch << 1) | done) and page-table entries per plane
+  // pop state ((epoch << 1) | done) and per request id {first page-table
+  // entry, entries per plane}
   const uint32_t *stack;
   int32_t *stack_top;
   uint32_t *pop_state;
-  const uint32_t *req_plane;
+  const uint32_t *req_geo;
   uint32_t epoch;  // this launch's pop epoch (>= 1)
   uint32_t pad0;
+  // All-layer launches (cp_attn_decode_layers): a request's layer cursor
+  // and the tokens its cursor has carried through every layer (both at
+  // index 2 * request id), and per launch entry the pieces finished so far
+  // (reset by the last one). ent_tag[r] is request id | layers << 20 for an
+  // entry whose completion moves a cursor, 0 otherwise.
+  uint32_t *layer_cursor;
+  uint32_t *layer_tokens;
+  uint32_t *entry_done;
   int32_t n_req, n_units;
   int32_t schedule;     // kSchedBalanced, kSchedQueue or kSchedGrid
   uint32_t total_cost;  // balanced: summed page costs of the launch
   GeomK geom[kMaxLaunchModels];
   DecReq req[kMaxReqPerLaunch];
+  uint32_t ent_tag[kMaxReqPerLaunch];
 };
+constexpr uint32_t kTagLayerShift = 20;
 
 // V columns one merge workgroup covers: 64 lanes of up to four columns
 // (d_v is 64, 128, 256 or 512).
@@ -175,7 +186,8 @@ struct StackPushArgs {
 
 static_assert(kMaxReqPerLaunch <= 64, "request lookups search one key per lane");
 static_assert(sizeof(StackPushArgs) <= 3072, "stack push arguments too large");
-static_assert(sizeof(DecodeArgs) <= 3584, "decode kernel arguments too large");
+// the argument segment (with the runtime's hidden arguments) stays under 4 KiB
+static_assert(sizeof(DecodeArgs) <= 3776, "decode kernel arguments too large");
 static_assert(sizeof(MergeArgs) <= 3072, "merge kernel arguments too large");
 static_assert(sizeof(AppendArgs) <= 3072, "append kernel arguments too large");
 

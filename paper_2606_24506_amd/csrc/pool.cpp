@@ -311,6 +311,12 @@ void PoolState::advance(int32_t id) {
   }
 }
 
+void PoolState::commit_token(int32_t id) {
+  Request &r = reqs_[id];
+  r.ctx_len += r.inflight;
+  r.inflight = 0;
+}
+
 int64_t PoolState::pages_to_grow(int32_t id, int64_t new_len) const {
   const Request &r = reqs_[id];
   int64_t need = ceil_div(new_len, P_);

@@ -150,6 +150,9 @@ class PoolState {
   // After a decode step at the request's cursor: moves to the next layer;
   // past the last one, commits the token in flight.
   void advance(int32_t id);
+  // After a launch that took the token in flight through every layer at
+  // once (the cursor stays at 0): commits it.
+  void commit_token(int32_t id);
   // Pages request id still needs (all planes) to reach new_len tokens.
   int64_t pages_to_grow(int32_t id, int64_t new_len) const;
   // Carves fresh chunks for a model until it has at least `pages` free page

@@ -54,8 +54,9 @@ __device__ __forceinline__ int unit_segment(const DecodeArgs &a, uint32_t u, Seg
 }
 
 // Device page stack (kAppPop; run by one thread): the first piece of this
-// launch to reach request rq's new page claims the request's pop, takes one
-// page per KV plane from the top of the model's stack and writes their
+// launch to reach request rq's new page (in any of its planes, when several
+// layers of the request share the launch) claims the request's pop, takes
+// one page per KV plane from the top of the model's stack and writes their
 // page-table entries (plane l gets the entry l below the top); any other
 // piece waits until the claimant has published them. The claimant waits on
 // nothing, so every wait ends. Returns the entry of the new page of the
@@ -69,10 +70,10 @@ __device__ __forceinline__ uint32_t pop_new_pages(const DecodeArgs &a, const Dec
   if (s != done) {
     if (s != claim && atomicCAS(st, s, claim) == s) {
       const int32_t L = g.layers;
-      const uint32_t plane = a.req_plane[rid];
+      const uint32_t base = a.req_geo[2 * rid], plane = a.req_geo[2 * rid + 1];
       const int32_t top = atomicSub(&a.stack_top[g.pool_model], L);
       const uint32_t *stk = a.stack + (uint64_t)g.pool_model * kStackCap;
-      for (int32_t l = 0; l < L; ++l) a.pte[rq.pte_base + (uint32_t)l * plane + pg] = stk[top - 1 - l];
+      for (int32_t l = 0; l < L; ++l) a.pte[base + (uint32_t)l * plane + pg] = stk[top - 1 - l];
       __hip_atomic_store(st, done, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
     } else {
       while (__hip_atomic_load(st, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT) != done) __builtin_amdgcn_s_sleep(1);
@@ -114,6 +115,26 @@ __device__ __forceinline__ void fused_append(const DecodeArgs &a, const DecReq &
   __syncthreads();
 }
 
+// Layer cursor of an all-layer launch (Section 3.2's per-batch layer
+// cursor and completion state, driven by the launch itself; run by one
+// thread after the piece's outputs or partials are written): the last of
+// the pieces of launch entry r (one KV layer of one request) moves the
+// request's cursor on by one layer; the one that completes the last layer
+// sets it back to 0 and counts the token as carried through every layer.
+__device__ __forceinline__ void piece_done(const DecodeArgs &a, int r) {
+  const DecReq &rq = a.req[r];
+  const uint32_t tag = a.ent_tag[r];
+  __threadfence();
+  const uint32_t pieces = (uint32_t)rq.n_chunks * rq.n_hblk;
+  if (atomicAdd(&a.entry_done[r], 1u) + 1 != pieces) return;
+  atomicExch(&a.entry_done[r], 0u);
+  const uint32_t rid = tag & ((1u << kTagLayerShift) - 1), layers = tag >> kTagLayerShift;
+  if (atomicAdd(&a.layer_cursor[2 * rid], 1u) + 1 == layers) {
+    atomicExch(&a.layer_cursor[2 * rid], 0u);
+    if (rq.app_flags & kAppRow) atomicAdd(&a.layer_tokens[2 * rid], 1u);
+  }
+}
+
 // Work loop of every decode kernel; `seg` is inlined once. Queue schedule:
 // workgroups pull unit indices from a device counter until the queue is
 // empty; the last workgroup to leave resets the counters for the next
@@ -149,7 +170,8 @@ __device__ __forceinline__ void decode_loop(const DecodeArgs &a, uint32_t *next,
     first = false;
     if (a.req[r].app_flags & kAppRow) fused_append(a, a.req[r], sg);
     seg(a.req[r], sg);
-    __syncthreads();  // LDS reuse by the next piece
+    __syncthreads();  // LDS reuse by the next piece; the piece's stores are issued
+    if (a.ent_tag[r] != 0 && threadIdx.x == 0) piece_done(a, r);
   }
   if (a.schedule == kSchedQueue && threadIdx.x == 0) {
     __threadfence();
