@@ -233,7 +233,10 @@ def measure(cfg: int, args) -> dict:
     del rows_full
     # one new token per request per step: seeded rows, resident on the GPU before timing
     new_rows = to_device_u16(np.concatenate([wl.step_rows_bits(r, 0).reshape(-1) for r in range(B)]), "cuda")
-    ones = [1] * B
+    # request ids and append counts marshalled once (the steps repeat them)
+    from paper_2606_24506_amd import crosspool as cpl
+    ones = cpl.i32_array([1] * B)
+    ids = [cpl.i32_array(ld.req_ids) for ld in lds]
     stream = torch.cuda.current_stream()
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
     for a, b in ev:
@@ -242,16 +245,21 @@ def measure(cfg: int, args) -> dict:
     torch.cuda.synchronize()
     opts = dict(num_splits=args.splits, path=args.path, schedule=args.schedule)
 
+    # device pointers and the stream handle taken once, as a serving loop
+    # would hold them
+    ptrs = [(ld.q.data_ptr(), ld.out.data_ptr(), ld.lse.data_ptr()) for ld in lds]
+    rows_p, stream_p = new_rows.data_ptr(), stream.cuda_stream
+
     def step(i, evs=None):
-        ld = lds[i % layers]
-        o = dict(opts)
+        ld, rid, (q_p, o_p, l_p) = lds[i % layers], ids[i % layers], ptrs[i % layers]
+        o = opts
         if evs is not None:
-            o.update(ev_begin=evs[0].cuda_event, ev_end=evs[1].cuda_event)
+            o = dict(opts, ev_begin=evs[0].cuda_event, ev_end=evs[1].cuda_event)
         if args.unfused:
-            ld.pool.append(ld.req_ids, ones, new_rows, stream)
-            ld.pool.decode(ld.req_ids, ld.q, ld.out, ld.lse, stream, **o)
+            ld.pool.append(rid, ones, rows_p, stream_p)
+            ld.pool.decode(rid, q_p, o_p, l_p, stream_p, **o)
         else:
-            ld.pool.decode_step(ld.req_ids, ones, new_rows, ld.q, ld.out, ld.lse, stream, **o)
+            ld.pool.decode_step(rid, ones, rows_p, q_p, o_p, l_p, stream_p, **o)
 
     if args.copy_mib:
         src = torch.empty(args.copy_mib << 20, dtype=torch.uint8, device="cuda")

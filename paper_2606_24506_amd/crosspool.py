@@ -139,13 +139,13 @@ def _load() -> C.CDLL:
         "cp_request_len": ([P, I32, C.POINTER(I64)], I32),
         "cp_request_cursor": ([P, I32, C.POINTER(I32), C.POINTER(I32)], I32),
         "cp_request_pages": ([P, I32, I64, I64, C.POINTER(C.c_uint32)], I32),
-        "cp_kv_append": ([P, I32, C.POINTER(I32), C.POINTER(I32), VP, VP], I32),
-        "cp_attn_decode": ([P, I32, C.POINTER(I32), VP, VP, VP, VP], I32),
-        "cp_attn_decode_ex": ([P, I32, C.POINTER(I32), VP, VP, VP, VP, C.POINTER(cp_decode_opts)], I32),
-        "cp_attn_decode_noalloc": ([P, I32, C.POINTER(I32), VP, VP, VP, VP, C.POINTER(cp_decode_opts)], I32),
-        "cp_attn_decode_step": ([P, I32, C.POINTER(I32), C.POINTER(I32), VP, VP, VP, VP, VP, C.POINTER(cp_decode_opts)],
+        "cp_kv_append": ([P, I32, VP, VP, VP, VP], I32),
+        "cp_attn_decode": ([P, I32, VP, VP, VP, VP, VP], I32),
+        "cp_attn_decode_ex": ([P, I32, VP, VP, VP, VP, VP, C.POINTER(cp_decode_opts)], I32),
+        "cp_attn_decode_noalloc": ([P, I32, VP, VP, VP, VP, VP, C.POINTER(cp_decode_opts)], I32),
+        "cp_attn_decode_step": ([P, I32, VP, VP, VP, VP, VP, VP, VP, C.POINTER(cp_decode_opts)],
                                 I32),
-        "cp_attn_decode_layers": ([P, I32, C.POINTER(I32), C.POINTER(I32), VP, VP, VP, VP, VP,
+        "cp_attn_decode_layers": ([P, I32, VP, VP, VP, VP, VP, VP, VP,
                                    C.POINTER(cp_decode_opts)], I32),
         "cp_request_layer_state": ([P, I32, C.POINTER(I32), C.POINTER(I64)], I32),
         "cp_kv_gather": ([P, I32, I64, I64, VP, VP], I32),
@@ -166,9 +166,21 @@ def _check(rc: int):
         raise CrossPoolError(rc, LIB.cp_last_error().decode(errors="replace"))
 
 
+def i32_array(xs: Sequence[int]):
+    """A host int32 array argument built once, for callers that repeat a
+    call with the same request ids (it is passed as it is)."""
+    return (C.c_int32 * len(xs))(*[int(x) for x in xs])
+
+
 def _i32_array(xs: Sequence[int]):
-    arr = (C.c_int32 * len(xs))(*[int(x) for x in xs])
-    return arr
+    """A host int32 array argument: an array from i32_array passes as it is,
+    a contiguous numpy int32 array passes its address (no copy), anything
+    else is copied into a ctypes array."""
+    if isinstance(xs, C.Array):
+        return xs
+    if isinstance(xs, np.ndarray) and xs.dtype == np.int32 and xs.flags.c_contiguous:
+        return xs.__array_interface__["data"][0]
+    return (C.c_int32 * len(xs))(*[int(x) for x in xs])
 
 
 def _ptr(t) -> Optional[int]:
@@ -180,6 +192,27 @@ def _ptr(t) -> Optional[int]:
     if not t.is_contiguous():
         raise ValueError("tensor must be contiguous")
     return t.data_ptr()
+
+
+_OPTS = {}
+
+
+def _event(e):
+    if e is None:
+        return None
+    return e.cuda_event if hasattr(e, "cuda_event") else int(e)
+
+
+def _opts(num_splits: int, schedule: int, path: int, ev_begin, ev_end):
+    """Pointer to a cp_decode_opts; the event-free ones are built once per
+    (num_splits, schedule, path) and reused."""
+    if ev_begin is None and ev_end is None:
+        key = (num_splits, schedule, path)
+        o = _OPTS.get(key)
+        if o is None:
+            o = _OPTS[key] = C.pointer(cp_decode_opts(num_splits, schedule, path, 0, None, None))
+        return o
+    return C.pointer(cp_decode_opts(num_splits, schedule, path, 0, _event(ev_begin), _event(ev_end)))
 
 
 def _stream(stream) -> Optional[int]:
@@ -278,57 +311,37 @@ def cp_attn_decode(pool: int, req_ids: Sequence[int], q, out, lse, stream=None) 
 def cp_attn_decode_ex(pool: int, req_ids: Sequence[int], q, out, lse, stream=None, *, num_splits: int = 0,
                       schedule: int = CP_SCHED_BALANCED, path: int = CP_PATH_AUTO, ev_begin=None,
                       ev_end=None) -> None:
-    def ev(e):
-        if e is None:
-            return None
-        return e.cuda_event if hasattr(e, "cuda_event") else int(e)
-
-    o = cp_decode_opts(num_splits, schedule, path, 0, ev(ev_begin), ev(ev_end))
+    o = _opts(num_splits, schedule, path, ev_begin, ev_end)
     _check(LIB.cp_attn_decode_ex(pool, len(req_ids), _i32_array(req_ids), _ptr(q), _ptr(out), _ptr(lse),
-                                 _stream(stream), C.byref(o)))
+                                 _stream(stream), o))
 
 
 def cp_attn_decode_noalloc(pool: int, req_ids: Sequence[int], q, out, lse, stream=None, *, num_splits: int = 0,
                            schedule: int = CP_SCHED_BALANCED, path: int = CP_PATH_AUTO, ev_begin=None,
                            ev_end=None) -> None:
-    def ev(e):
-        if e is None:
-            return None
-        return e.cuda_event if hasattr(e, "cuda_event") else int(e)
-
-    o = cp_decode_opts(num_splits, schedule, path, 0, ev(ev_begin), ev(ev_end))
+    o = _opts(num_splits, schedule, path, ev_begin, ev_end)
     _check(LIB.cp_attn_decode_noalloc(pool, len(req_ids), _i32_array(req_ids), _ptr(q), _ptr(out), _ptr(lse),
-                                      _stream(stream), C.byref(o)))
+                                      _stream(stream), o))
 
 
 def cp_attn_decode_step(pool: int, req_ids: Sequence[int], n_new: Sequence[int], rows, q, out, lse, stream=None, *,
                         num_splits: int = 0, schedule: int = CP_SCHED_BALANCED, path: int = CP_PATH_AUTO,
                         ev_begin=None, ev_end=None) -> None:
-    def ev(e):
-        if e is None:
-            return None
-        return e.cuda_event if hasattr(e, "cuda_event") else int(e)
-
     n = len(req_ids)
     if len(n_new) != n:
         raise ValueError("req_ids and n_new differ in length")
-    o = cp_decode_opts(num_splits, schedule, path, 0, ev(ev_begin), ev(ev_end))
+    o = _opts(num_splits, schedule, path, ev_begin, ev_end)
     _check(LIB.cp_attn_decode_step(pool, n, _i32_array(req_ids), _i32_array(n_new), _ptr(rows), _ptr(q), _ptr(out),
-                                   _ptr(lse), _stream(stream), C.byref(o)))
+                                   _ptr(lse), _stream(stream), o))
 
 
 def cp_attn_decode_layers(pool: int, req_ids: Sequence[int], n_new: Sequence[int], rows, q, out, lse, stream=None, *,
                           num_splits: int = 0, schedule: int = CP_SCHED_BALANCED, path: int = CP_PATH_AUTO,
                           ev_begin=None, ev_end=None) -> None:
-    def ev(e):
-        if e is None:
-            return None
-        return e.cuda_event if hasattr(e, "cuda_event") else int(e)
-
-    o = cp_decode_opts(num_splits, schedule, path, 0, ev(ev_begin), ev(ev_end))
+    o = _opts(num_splits, schedule, path, ev_begin, ev_end)
     n = len(req_ids)
     _check(LIB.cp_attn_decode_layers(pool, n, _i32_array(req_ids), _i32_array(n_new), _ptr(rows), _ptr(q), _ptr(out),
-                                     _ptr(lse), _stream(stream), C.byref(o)))
+                                     _ptr(lse), _stream(stream), o))
 
 
 def cp_request_layer_state(pool: int, req_id: int):
