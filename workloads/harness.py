@@ -58,7 +58,7 @@ def to_device_u16(arr: np.ndarray, device):
 def load(wl: Workload, device: int = 0, *, placement_seed: Optional[int] = None, reserve_extra: int = 0,
          interleave: int = 0, rows_override: Optional[Dict[int, np.ndarray]] = None,
          q_override: Optional[List[np.ndarray]] = None, chunk_rows: int = 1 << 17, backing: int = 0,
-         n_layers: int = 1, device_pages: int = 0) -> Loaded:
+         n_layers: int = 1, device_pages: int = 0, page_tokens: int = PAGE_TOKENS) -> Loaded:
     """Build a pool holding the workload.
 
     interleave > 0 appends rows in rounds of `interleave` tokens per request,
@@ -67,7 +67,8 @@ def load(wl: Workload, device: int = 0, *, placement_seed: Optional[int] = None,
     backing selects the pool's memory (0 one buffer, 1 virtual ranges).
     n_layers > 1 registers the models with that many KV planes, each holding
     the same rows. device_pages = 1 gives the models device free-page stacks
-    (decode steps take new pages on the device).
+    (decode steps take new pages on the device). page_tokens sets the pool's
+    page size (tokens per page).
     """
     import torch
 
@@ -75,7 +76,7 @@ def load(wl: Workload, device: int = 0, *, placement_seed: Optional[int] = None,
 
     dev = torch.device("cuda", device)
     seed = wl.placement_seed if placement_seed is None else placement_seed
-    pool = cpl.Pool(page_tokens=PAGE_TOKENS, pool_bytes=wl.pool_bytes, chunk_bytes=wl.chunk_bytes,
+    pool = cpl.Pool(page_tokens=page_tokens, pool_bytes=wl.pool_bytes, chunk_bytes=wl.chunk_bytes,
                     placement_seed=seed, device=device, backing=backing, device_pages=device_pages)
     mids = {name: pool.register_spec(MODELS[name], n_layers=n_layers) for name in wl.models_used()}
     if wl.filler_model and wl.filler_model not in mids:
@@ -89,12 +90,12 @@ def load(wl: Workload, device: int = 0, *, placement_seed: Optional[int] = None,
     left = wl.filler_pages
     while left > 0:
         take = min(256, left)
-        fillers.append(pool.open(mids[wl.filler_model], take * PAGE_TOKENS))
+        fillers.append(pool.open(mids[wl.filler_model], take * page_tokens))
         fcap.append(take)
         left -= take
     filler_page = None
     if fillers:
-        filler_page = torch.zeros((n_layers, PAGE_TOKENS, MODELS[wl.filler_model].row_width), dtype=torch.int16,
+        filler_page = torch.zeros((n_layers, page_tokens, MODELS[wl.filler_model].row_width), dtype=torch.int16,
                                   device=dev)
 
     def rows_of(r):
@@ -112,7 +113,7 @@ def load(wl: Workload, device: int = 0, *, placement_seed: Optional[int] = None,
             torch.cuda.synchronize(dev)
         for f, cap in zip(fillers, fcap):
             for _ in range(cap):
-                pool.append([f], [PAGE_TOKENS], filler_page)
+                pool.append([f], [page_tokens], filler_page)
     else:
         all_rows = [rows_of(r) for r in range(len(rids))]
         pos = [0] * len(rids)
@@ -131,7 +132,7 @@ def load(wl: Workload, device: int = 0, *, placement_seed: Optional[int] = None,
                 pool.append(ids, nn, to_device_u16(np.concatenate(blocks), dev))
             for i, f in enumerate(fillers):
                 if fpos[i] < fcap[i]:
-                    pool.append([f], [PAGE_TOKENS], filler_page)
+                    pool.append([f], [page_tokens], filler_page)
                     fpos[i] += 1
     torch.cuda.synchronize(dev)
 
