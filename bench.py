@@ -82,6 +82,8 @@ def parse():
                          "(reported under layer_launch)")
     ap.add_argument("--device-pages", action="store_true",
                     help="pools with device free-page stacks: the steps pop new pages inside the launch")
+    ap.add_argument("--no-inflight", action="store_true",
+                    help="skip the two-batches-in-flight record (two pools stepping on two streams)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="target CPU time of the oracle sample")
     ap.add_argument("--copy-mib", type=int, default=0,
@@ -457,6 +459,111 @@ def measure_layer_launch(cfg: int, args) -> dict:
                     "cp_attn_decode_layers call", **rec}
 
 
+_STREAMS = []
+
+
+def inflight_streams():
+    """The two streams of the in-flight passes, made once per process (at
+    the default priority) and reused by every workload: HIP maps streams
+    onto a few hardware queues, and two streams that share one run their
+    launches in turn."""
+    import torch
+
+    if not _STREAMS:
+        _STREAMS.extend([torch.cuda.Stream(), torch.cuda.Stream()])
+    return _STREAMS
+
+
+def measure_inflight(cfg: int, args) -> dict:
+    """Two batches in flight (the layer-wise pipeline keeps two batches,
+    each with its own state, in flight; Section 3.2): two pools, each
+    holding a copy of the workload, their decode steps issued alternately on
+    two streams, against the same steps issued on one stream. Each pool
+    stays on one stream; each batch cycles enough pools that the two
+    together hold over 1 GiB of KV. Returns aggregate whole-step GB/s."""
+    import torch
+
+    from workloads import make_workload
+    from workloads.harness import load, to_device_u16
+    from paper_2606_24506_amd import crosspool as cpl
+
+    wl = make_workload(cfg, scale_ctx=args.ctx_scale)
+    if args.ctx_scale != 1.0 and wl.filler_pages:
+        wl.filler_pages = int(wl.filler_pages * args.ctx_scale)
+    B = len(wl.requests)
+    kv_bytes = sum(rq.ctx_len * wl.model(r).kappa for r, rq in enumerate(wl.requests))
+    lay = max(1, math.ceil((1 << 29) / kv_bytes))  # pools per batch
+    K = max(2, args.steps)  # step pairs per timed pass
+    warm = max(2, args.steps)
+    visits_per_pool = -(-(2 * warm + 4 * K) // lay) + 2
+    inter = 512 if cfg == 4 else (4096 if cfg == 5 else 0)
+    pools = [[load(wl, reserve_extra=visits_per_pool, interleave=inter,
+                   placement_seed=wl.placement_seed + 1000 * (b * lay + li) + 7) for li in range(lay)]
+             for b in range(2)]
+    new_rows = to_device_u16(np.concatenate([wl.step_rows_bits(r, 0).reshape(-1) for r in range(B)]), "cuda")
+    ones = cpl.i32_array([1] * B)
+    ids = [[cpl.i32_array(ld.req_ids) for ld in row] for row in pools]
+    ptrs = [[(ld.q.data_ptr(), ld.out.data_ptr(), ld.lse.data_ptr()) for ld in row] for row in pools]
+    streams = inflight_streams()
+    sp = [st.cuda_stream for st in streams]
+    rows_p = new_rows.data_ptr()
+    visits = [[0] * lay for _ in range(2)]
+
+    def pair(j, two, seen):
+        for b in (0, 1):
+            li = j % lay
+            q_p, o_p, l_p = ptrs[b][li]
+            pools[b][li].pool.decode_step(ids[b][li], ones, rows_p, q_p, o_p, l_p, sp[b] if two else sp[0])
+            visits[b][li] += 1
+            seen.append(visits[b][li])
+
+    def bytes_of(seen):  # counted after the timed pass, off the host's issue path
+        return sum(algorithmic_bytes_decode(wl, [rq.ctx_len + v for rq in wl.requests]) for v in seen)
+
+    # clock settling as in measure(): decode-only calls (no context grows)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    n_settle = 0
+    while time.perf_counter() - t0 < args.settle_seconds and n_settle < MAX_SETTLE_CALLS:
+        for row in pools:
+            for ld in row:
+                ld.pool.decode(ld.req_ids, ld.q, ld.out, ld.lse, streams[0])
+        n_settle += 1
+        if n_settle % 8 == 0:
+            streams[0].synchronize()
+    # warmup, one pass in each mode: the first pass on two streams runs
+    # slower than later ones (measured 5-10% on the V2-Lite batch), a one-time
+    # cost of the second stream's first use
+    j = 0
+    for two in (False, True):
+        for _ in range(warm):
+            pair(j, two, [])
+            j += 1
+        torch.cuda.synchronize()
+    rates = {1: [], 2: []}
+    for two in (False, True, False, True):
+        seen = []
+        t0 = time.perf_counter()
+        for _ in range(K):
+            pair(j, two, seen)
+            j += 1
+        for st in streams:
+            st.synchronize()
+        dt = time.perf_counter() - t0
+        rates[2 if two else 1].append(bytes_of(seen) / dt / 1e9)
+        log(f"cfg{cfg}: in-flight pass on {'two streams' if two else 'one stream'}: {rates[2 if two else 1][-1]:.0f} GB/s")
+    for row in pools:
+        for ld in row:
+            ld.close()
+    torch.cuda.empty_cache()
+    one, two = sum(rates[1]) / 2, sum(rates[2]) / 2
+    log(f"cfg{cfg}: two batches in flight {two:.0f} GB/s against {one:.0f} GB/s on one stream")
+    return {"workload": "two batches of " + WORKLOAD_NAMES[cfg],
+            "step": "cp_attn_decode_step (1 appended token/request + decode) on each batch's pool in turn",
+            "two_streams_GBps": round(two, 2), "one_stream_GBps": round(one, 2),
+            "ratio": round(two / one, 4), "pools_per_batch": lay, "step_pairs_per_pass": K}
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -476,7 +583,12 @@ def main():
     else:
         also = [int(x) for x in args.also.split(",") if x and int(x) != args.config]
 
+    inflight_ok = not args.no_inflight and not (args.planes or args.unfused or args.device_pages or args.backing)
+    if inflight_ok:
+        inflight_streams()
     head = measure(args.config, args)
+    if inflight_ok:
+        head["two_batches_in_flight"] = measure_inflight(args.config, args)
     per_config = {}
     for c in also:
         r = measure(c, args)
@@ -485,6 +597,8 @@ def main():
                               "host_enqueue_ms_per_step": r["host_enqueue_ms_per_step"],
                               "roofline": r["roofline"], "whole_step": r["whole_step"], "matrix": r["matrix"],
                               "config": r["config"]}
+        if inflight_ok:
+            per_config[str(c)]["two_batches_in_flight"] = measure_inflight(c, args)
     res = {
         "metric": "paged decode-attention achieved HBM GB/s and req-tokens/s on 1 MI355X",
         "value": head["value"],
@@ -507,6 +621,8 @@ def main():
         "matrix": head["matrix"],
         "per_config": per_config,
     }
+    if "two_batches_in_flight" in head:
+        res["two_batches_in_flight"] = head["two_batches_in_flight"]
     if args.layer_launch:
         res["layer_launch"] = measure_layer_launch(2 if args.config == 3 else args.config, args)
     if not args.no_cpu_baseline:

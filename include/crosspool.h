@@ -38,6 +38,9 @@
  *   - A pool is not thread-safe: the caller serialises calls on one pool.
  *     Decode calls on one pool must not overlap on the GPU (one stream, or
  *     the caller orders streams), because they share the pool's workspace.
+ *     Different pools share no device state: their calls may run at the
+ *     same time on different streams (two batches in flight, Section 3.2).
+ *     cp_attn_decode_noalloc is the exception: its workspace is per GPU.
  *   - bf16 is IEEE-754 binary32 truncated to its upper 16 bits; values are
  *     produced with round-to-nearest-even.
  */
