@@ -5,8 +5,9 @@ here) and the narrow and small-group kernels pages of a multiple of 16;
 other sizes go to the generic vector kernel. Each size runs a ragged batch
 of every kernel family (contexts of one token, one short of and one past a
 page or tile boundary, several pages) under the balanced schedule and under
-forced splits, and fused decode steps that open new pages, all against the
-fp64 oracle at the usual bars."""
+forced splits, fused decode steps that open new pages, and unsplit pieces
+long enough to reload the page-table entries several times, all against
+the fp64 oracle at the usual bars."""
 import math
 
 import numpy as np
@@ -73,5 +74,26 @@ def test_fused_steps_at_page_size(page_tokens):
                     f"step at page size {page_tokens}")
         for r, rid in enumerate(ld.req_ids):
             assert ld.pool.ctx_len(rid) == rows_now[r].shape[0]
+    finally:
+        ld.close()
+
+
+@pytest.mark.parametrize("page_tokens", [32, 64])
+def test_long_unsplit_pieces(page_tokens):
+    """One piece per request (one forced KV range) over 70 to 290 pages:
+    every kernel family reloads its batch of 64 page-table entries several
+    times inside one piece."""
+    print(f"[case] long unsplit pieces at page size {page_tokens}", flush=True)
+    specs = [("mla128", 9000), ("mla16", 9001), ("mqa32", 5000), ("gqa32x4", 4500), ("gqa16x4d64", 4200),
+             ("mqa128", 4300)]
+    rng = np.random.default_rng(77)
+    reqs = [RequestSpec(m, n) for m, n in specs]
+    qs = [normal_bf16(rng, (MODELS[m].n_q_heads, MODELS[m].d_k), 1.0) for m, _ in specs]
+    wl = Workload(f"long{page_tokens}", 13, reqs, qs, math.sqrt(0.5), 512 << 20, 2 << 20, 13)
+    ld = load(wl, interleave=97, page_tokens=page_tokens)
+    try:
+        ld.decode(num_splits=1, schedule=cpl.CP_SCHED_QUEUE)
+        torch.cuda.synchronize()
+        compare(ld, {r: expected_for(wl, r) for r in range(len(specs))}, f"long unsplit pieces P{page_tokens}")
     finally:
         ld.close()
