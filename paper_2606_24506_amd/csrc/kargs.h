@@ -49,9 +49,10 @@ enum : int32_t {
 constexpr bool is_wide_variant(int v) { return v == kM_MLA_G128 || v == kM_D128_G64 || v == kM_D128_G128; }
 
 // One piece of decode work: pages [pg_begin, pg_end) of a request, for one
-// head block, writing partial slot `slot` when the request is split.
+// head block, writing partial slot `slot` when the request is split; model
+// is the request's index into DecodeArgs::geom.
 struct Seg {
-  uint32_t pg_begin, pg_end, slot, hblk;
+  uint32_t pg_begin, pg_end, slot, hblk, model;
 };
 
 // Per-model geometry as the kernels see it.

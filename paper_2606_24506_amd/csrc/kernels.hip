@@ -317,7 +317,7 @@ constexpr int kernel_lds_bytes(uint32_t mask) {
 
 template <uint32_t MASK>
 __device__ __forceinline__ void run_seg(const DecodeArgs &a, const DecReq &rq, const Seg &sg, char *lds) {
-  const GeomK &gm = a.geom[rq.model];
+  const GeomK &gm = a.geom[sg.model];
 #define CP_VCASE(V, HB, DPL)                                        \
   if constexpr (has(MASK, V)) {                                     \
     if (gm.variant == V) {                                          \

@@ -13,30 +13,46 @@
 namespace cp {
 
 // Finds the next piece of work of this workgroup for the balanced
-// schedule, starting the search at request *r, head block *hb. Returns
-// false when the workgroup's share is exhausted.
+// schedule: head block *hb or a later one of request *r, or the first head
+// block of a later request, whose pages meet the workgroup's share
+// [L0, L1) of the cost line (page j of a request sits at its cost position
+// plus j times its model's page cost). Lane i evaluates request i: one
+// round of loads from the argument segment (the models' page sizes and
+// costs are uniform loads) and one ballot, so that the first piece of a
+// launch starts after a single round trip. All arithmetic fits 32 bits:
+// the host keeps the cost line below 2^32 and the grid below 2^16.
+// Returns false when the workgroup's share is exhausted.
 __device__ __forceinline__ bool next_balanced(const DecodeArgs &a, int *r, uint32_t *hb, Seg *sg) {
-  const uint64_t W = gridDim.x, w = blockIdx.x, T = a.total_cost;
-  const uint64_t L0 = w * T / W, L1 = (w + 1) * T / W;
-  for (; *r < a.n_req; ++*r, *hb = 0) {
-    const DecReq &rq = a.req[*r];
-    const GeomK &gm = a.geom[rq.model];
-    // the request's pages start at its cost prefix (any fixed cost of a
-    // piece that starts there comes before it)
-    const uint64_t c = (uint64_t)gm.page_cost, C = rq.unit_begin;
-    if (C >= L1) return false;
-    const uint64_t pages = (rq.ctx_len + gm.page_tokens - 1) / gm.page_tokens;
-    if (C + pages * c <= L0) continue;
-    const uint64_t jb = L0 > C ? (L0 - C + c - 1) / c : 0;
-    const uint64_t je = min(pages, (L1 - C + c - 1) / c);
-    if (jb >= je || *hb >= rq.n_hblk) continue;
-    sg->pg_begin = (uint32_t)jb;
-    sg->pg_end = (uint32_t)je;
-    sg->slot = (uint32_t)(w - rq.chunk_pages);
-    sg->hblk = *hb;
-    return true;
+  const uint32_t W = gridDim.x, w = blockIdx.x, T = a.total_cost;
+  const uint32_t q = T / W, rm = T % W;  // floor(w T / W) = w q + floor(w rm / W), and w rm < 2^32
+  const uint32_t L0 = w * q + w * rm / W, L1 = (w + 1) * q + (w + 1) * rm / W;
+  const int i = threadIdx.x & 63;
+  const DecReq &ri = a.req[i < a.n_req ? i : 0];
+  const uint32_t C = ri.unit_begin, model = ri.model, nh = ri.n_hblk;
+  uint32_t P = (uint32_t)a.geom[0].page_tokens, c = (uint32_t)a.geom[0].page_cost;
+#pragma unroll
+  for (int m = 1; m < kMaxLaunchModels; ++m)
+    if (model == (uint32_t)m) {
+      P = (uint32_t)a.geom[m].page_tokens;
+      c = (uint32_t)a.geom[m].page_cost;
+    }
+  const uint32_t pages = (ri.ctx_len + P - 1) / P;
+  const uint32_t jb = L0 > C ? (L0 - C + c - 1) / c : 0u;
+  const uint32_t je = C < L1 ? min(pages, (L1 - C + c - 1) / c) : 0u;
+  const bool ok = i < a.n_req && i >= *r && jb < je && (i > *r || *hb < nh);
+  const uint64_t b = __builtin_amdgcn_ballot_w64(ok);
+  if (b == 0) return false;
+  const int k = __builtin_ctzll(b);
+  if (k != *r) {
+    *r = k;
+    *hb = 0;
   }
-  return false;
+  sg->pg_begin = __builtin_amdgcn_readlane(jb, k);
+  sg->pg_end = __builtin_amdgcn_readlane(je, k);
+  sg->slot = w - __builtin_amdgcn_readlane((uint32_t)ri.chunk_pages, k);
+  sg->hblk = *hb;
+  sg->model = __builtin_amdgcn_readlane(model, k);
+  return true;
 }
 
 // Decodes unit u of the queue and grid schedules into (request, piece).
@@ -50,6 +66,7 @@ __device__ __forceinline__ int unit_segment(const DecodeArgs &a, uint32_t u, Seg
   sg->pg_end = min(pages, sg->pg_begin + rq.chunk_pages);
   sg->slot = chunk;
   sg->hblk = local % rq.n_hblk;
+  sg->model = rq.model;
   return r;
 }
 
@@ -91,7 +108,7 @@ __device__ __forceinline__ uint32_t pop_new_pages(const DecodeArgs &a, const Dec
 // the same bytes, which is harmless; each one's own stores precede its
 // loads through the workgroup barrier.
 __device__ __forceinline__ void fused_append(const DecodeArgs &a, const DecReq &rq, const Seg &sg) {
-  const GeomK &g = a.geom[rq.model];
+  const GeomK &g = a.geom[sg.model];
   const uint32_t P = (uint32_t)g.page_tokens;
   const uint32_t pos = rq.ctx_len - 1, pg = pos / P;
   if (pg < sg.pg_begin || pg >= sg.pg_end) return;
@@ -141,12 +158,7 @@ __device__ __forceinline__ void piece_done(const DecodeArgs &a, int r) {
 // launch.
 template <class F>
 __device__ __forceinline__ void decode_loop(const DecodeArgs &a, uint32_t *next, F &&seg) {
-  // balanced: request being searched, starting with the one that holds the
-  // first cost unit of this workgroup's share
-  int br = a.schedule == kSchedBalanced
-               ? sorted_search(a.n_req, (uint64_t)blockIdx.x * a.total_cost / gridDim.x,
-                               [&](int i) { return a.req[i].unit_begin; })
-               : 0;
+  int br = 0;        // balanced: request of the last piece
   uint32_t bhb = 0;  // balanced: next head block of that request
   bool first = true;
   for (;;) {

@@ -20,7 +20,7 @@ template <> struct WideVar<kM_D128_G128> { static constexpr int G = 128, DK = 12
 __global__ __launch_bounds__(64 * MlaCfg::NW, 1) void decode_mla_kernel(const DecodeArgs a) {
   __shared__ __attribute__((aligned(16))) char lds[MlaCfg::LDS];
   __shared__ uint32_t next;
-  decode_loop(a, &next, [&](const DecReq &rq, const Seg &sg) { mla_unit(a, a.geom[rq.model], rq, sg, lds); });
+  decode_loop(a, &next, [&](const DecReq &rq, const Seg &sg) { mla_unit(a, a.geom[sg.model], rq, sg, lds); });
 }
 
 // One workgroup of four waves per CU; every request of the launch uses
@@ -32,7 +32,7 @@ __global__ __launch_bounds__(64 * WideVar<V>::NW, 1) void decode_wide_kernel(con
   __shared__ __attribute__((aligned(16))) char lds[C::LDS];
   __shared__ uint32_t next;
   decode_loop(a, &next, [&](const DecReq &rq, const Seg &sg) {
-    wide_unit<W::G, W::DK, W::DV, W::MLA, W::QL, W::NW>(a, a.geom[rq.model], rq, sg, lds);
+    wide_unit<W::G, W::DK, W::DV, W::MLA, W::QL, W::NW>(a, a.geom[sg.model], rq, sg, lds);
   });
 }
 
