@@ -113,8 +113,10 @@ CP_DEV bf16x8 mla_vfrag(const char *vslot, const LaneIds &L, int b) {
 // Flag bytes of a rescale record, the same in every lane.
 CP_DEV uint64_t mla_flags(const char *xrec) {
   const uint64_t f = *reinterpret_cast<const uint64_t *>(xrec);
-  return ((uint64_t)__builtin_amdgcn_readfirstlane((uint32_t)(f >> 32)) << 32) |
-         __builtin_amdgcn_readfirstlane((uint32_t)f);
+  // the builtin returns a signed int: both halves are zero-extended
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)f);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(f >> 32));
+  return ((uint64_t)hi << 32) | lo;
 }
 
 __device__ __forceinline__ void mla_unit(const DecodeArgs &a, const GeomK &gm, const DecReq &rq, const Seg &sg,
