@@ -178,27 +178,53 @@ __device__ __forceinline__ void narrow_unit(const DecodeArgs &a, const GeomK &gm
   const int vrow = 4 * quad + (col >> 2);  // V row this lane supplies to a transpose read
   const int vcol = 8 * (col & 3) + 32 * nb0;
 
-  // Unit start: the page-table entries, then the first slice's loads, then
-  // the query, so that the latencies of the last two overlap.
-  if (NSLOT == 2 && mine > 0) issue(0);
-  // Q^T operand fragments: lane holds head (h0 + 16 hb + col), dims
-  // 32 c + 8 quad .. +7 (zero for padded head columns).
-  bf16x8 qf[C::HBW][C::KSTEPS];
-#pragma unroll
-  for (int hb = 0; hb < C::HBW; ++hb) {
-    const int hh = 16 * hb + col;
-    const uint16_t *qrow = a.q + rq.q_off + (uint32_t)(h0 + (hh < hv ? hh : 0)) * DK + 8 * quad;
-#pragma unroll
-    for (int c = 0; c < C::KSTEPS; ++c) {
-      bf16x8 v = *reinterpret_cast<const bf16x8 *>(qrow + 32 * c);
-      if (hh >= hv) v = bf16x8{};
-      qf[hb][c] = v;
-      // a long query lives in the accumulation registers, which the matrix
-      // cores read directly as the B operand; that leaves the architectural
-      // registers to the accumulators and to fragment prefetch
-      if constexpr (C::AGPR_Q) asm volatile("" : "+a"(qf[hb][c]));
+  // Unit start. The query is staged through LDS: its Q^T operand fragments
+  // (lane holds head h0 + 16 hb + col, dims 32 c + 8 quad .. +7) are copied
+  // by direct loads into a second ring slot in fragment order (fragment
+  // f = hb KSTEPS + c at byte 1024 f + 16 lane). When the streams share the
+  // unit's heads, one copy in stream 0's slot serves the workgroup and
+  // every wave copies every NW-th fragment; when each stream owns a KV head
+  // (and so its own h0), each stream copies its query into its own slot.
+  // Those loads read 16 rows of 64 bytes each, which the address unit
+  // serves a row at a time, so one copy per workgroup (or stream) instead
+  // of one per wave keeps them from delaying the first slice. The
+  // page-table wait of the first slice's issue covers the copy; the slot is
+  // free until the loop's first barrier, by which point every wave has read
+  // its fragments.
+  constexpr int NQF = C::HBW * C::KSTEPS;
+  static_assert(NQF * 1024 <= C::SLICE, "the query fits one ring slot");
+  static_assert(NSLOT == 2, "the query is staged in the second ring slot");
+  char *const qstage = (head_par ? ring : lds) + C::SLICE;
+  {
+    const int qw = head_par ? member : wave, nqw = head_par ? SHARE : NW;  // this copier, copiers
+    const uint64_t qb = uniform_ptr(a.q + rq.q_off + (uint32_t)h0 * DK) - kDmaBias;
+    for (int f = qw; f < NQF; f += nqw) {
+      const int hb = f / C::KSTEPS, c = f - hb * C::KSTEPS, hh = 16 * hb + col;
+      const uint32_t o[4] = {(uint32_t)((hh < hv ? hh : 0) * DK + 32 * c + 8 * quad) * 2 + kDmaBias, 0u, 0u, 0u};
+      dma_group<1>(qb, o, lds_addr(qstage + 1024 * f));
     }
   }
+  if (mine > 0) issue(0);
+  else wait_vm<0>();
+  __syncthreads();  // the query copy is visible to every wave
+  bf16x8 qf[C::HBW][C::KSTEPS];
+#pragma unroll
+  for (int hb = 0; hb < C::HBW; ++hb)
+#pragma unroll
+    for (int c = 0; c < C::KSTEPS; ++c)
+      qf[hb][c] = *reinterpret_cast<const bf16x8 *>(qstage + 1024 * (hb * C::KSTEPS + c) + 16 * lane);
+#pragma unroll
+  for (int hb = 0; hb < C::HBW; ++hb)
+#pragma unroll
+    for (int c = 0; c < C::KSTEPS; ++c) {
+      if (16 * hb + col >= hv) qf[hb][c] = bf16x8{};
+      // a long query lives in the accumulation registers, which the matrix
+      // cores read directly as the B operand; that leaves the architectural
+      // registers to the accumulators and to fragment prefetch. Either way
+      // the reads complete here, before the slot is refilled.
+      if constexpr (C::AGPR_Q) asm volatile("" : "+a"(qf[hb][c]));
+      else asm volatile("" : "+v"(qf[hb][c]));
+    }
 
 #pragma unroll 1
   for (int i = 0; i < iters; ++i) {
