@@ -14,7 +14,7 @@ attention families that share the pool are GQA, MQA and MLA (Section 1 and
 Section 2.2). This module writes that definition out directly, in float64,
 over contiguous rows; it never sees pages.
 
-Readings taken where the paper is silent (listed in the design doc as well):
+Readings taken where the paper is silent:
   * MLA caches one latent head per token, [latent | rope]; K is the whole
     row, V is its first ``latent_dim`` entries; the query arrives already
     absorbed (its no-rope part multiplied through W_UK) and post-rope.

@@ -23,7 +23,7 @@ def _has_gpu() -> bool:
 
 
 def pytest_collection_modifyitems(config, items):
-    # GPU tests are skipped only when no GPU is visible at all. On a GPU machine a
+    # GPU tests are skipped only when no GPU is visible at all. With a GPU, a
     # missing or broken HIP library makes them fail loudly instead.
     if _has_gpu():
         return
